@@ -1,0 +1,11 @@
+"""Test infrastructure only: a plain float64 CPU forward of the dense decoder.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg use this
+package.  It shares no code with the GPU path and imports nothing from it.
+"""
+
+from .model import (DecoderOracle, attend, bf16_round, greedy, rms_norm, rope_rotate,
+                    silu, softmax)
+
+__all__ = ["DecoderOracle", "attend", "bf16_round", "greedy", "rms_norm", "rope_rotate",
+           "silu", "softmax"]
