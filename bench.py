@@ -1,0 +1,205 @@
+"""Benchmark: batch-1 decode tokens/s and prefill TTFT of the HIP path on one GPU.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 8b]
+
+One step = one request of the workload: reset the KV cache, prefill the prompt
+(TTFT), then the configured number of greedy decode steps.  Inputs (weights,
+prompt ids) are seeded synthetic data generated on the host and uploaded once,
+before the timed region.  Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12          # MI355X HBM3E, bytes/s
+MFMA_BF16_PEAK = 2.5e15    # MI355X dense bf16 matrix peak, flop/s
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def run_request(model, prompt, n_decode):
+    model.reset_kv()
+    t0 = time.perf_counter()
+    tok, _ = model.prefill(prompt)
+    t1 = time.perf_counter()
+    for _ in range(n_decode):
+        model.decode_step(-1)
+    t2 = time.perf_counter()
+    return t1 - t0, t2 - t1, tok
+
+
+def gateup_bytes(cfg) -> int:
+    """Algorithmic HBM bytes of one gate/up GEMV launch: both weight matrices once,
+    the input vector and norm gain read, the SwiGLU output written."""
+    return 2 * cfg.ffn_dim * cfg.d_model * cfg.wbytes + 2 * cfg.d_model * 4 + cfg.ffn_dim * 4
+
+
+def profile_pass(model, cfg, prompt, n_decode):
+    """Eager decode steps with HIP events around every launch (same positions as a
+    timed request).  Returns mean per-launch ms per kernel class and per-token sums."""
+    model.reset_kv()
+    model.prefill(prompt)
+    L = cfg.n_layers
+    acc = {k: [] for k in ("embed", "qkv", "attn", "o", "gateup", "down", "lm_head", "argmax")}
+    for _ in range(n_decode):
+        _, dur = model.profile_decode_step(-1)
+        acc["embed"].append(dur[0])
+        per = dur[1:1 + 5 * L].reshape(L, 5)
+        for j, k in enumerate(("qkv", "attn", "o", "gateup", "down")):
+            acc[k].extend(per[:, j].tolist())
+        acc["lm_head"].append(dur[1 + 5 * L])
+        acc["argmax"].append(dur[2 + 5 * L])
+    mean = {k: float(np.mean(v)) for k, v in acc.items()}
+    per_token = {k: float(np.sum(v)) / n_decode for k, v in acc.items()}
+    return mean, per_token
+
+
+def cpu_baseline(cfg, w, n_prompt, n_decode):
+    """The float64 oracle on the host cores over a bounded sample of the workload
+    (a shorter prompt, a few decode steps); returns the sample's ids and logits so
+    the GPU path can be compared with it."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import DecoderOracle, greedy
+    from paper_2608_24204_amd import inputs
+    t0 = time.perf_counter()
+    w64 = inputs.weights_f64(cfg, w)
+    conv_s = time.perf_counter() - t0
+    prompt = inputs.make_prompt(cfg, n_prompt)
+    orc = DecoderOracle(cfg, w64, max_seq=n_prompt + n_decode + 1)
+    t0 = time.perf_counter()
+    lg = orc.prefill(prompt)
+    t1 = time.perf_counter()
+    ids, logs = [greedy(lg)], [lg]
+    for _ in range(n_decode):
+        lg = orc.decode(ids[-1])
+        ids.append(greedy(lg))
+        logs.append(lg)
+    t2 = time.perf_counter()
+    threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    out = {"value": n_decode / (t2 - t1), "unit": "tokens/s", "cores": int(threads),
+           "kind": "oracle",
+           "sample": f"{cfg.name}: prefill of {n_prompt} prompt ids then {n_decode} greedy decode "
+                     f"steps, float64 numpy on the host (weights widened to float64 beforehand, "
+                     f"{conv_s:.1f} s, not timed)",
+           "prefill_tok_s": n_prompt / (t1 - t0), "ttft_ms": (t1 - t0) * 1e3,
+           "host_cpus": os.cpu_count()}
+    return out, (prompt, ids, logs)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="8b")
+    ap.add_argument("--decode", type=int, default=None, help="override decode steps per request")
+    ap.add_argument("--prefill-mode", default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--cpu-prompt", type=int, default=128)
+    ap.add_argument("--cpu-decode", type=int, default=3)
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(this build has no multi-GPU path)", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2608_24204_amd import binding, configs, inputs
+    cfg = configs.CONFIGS[args.config]
+    n_decode = cfg.decode_steps if args.decode is None else args.decode
+    log(f"config {cfg.name}: generating weights")
+    t0 = time.perf_counter()
+    w = inputs.make_weights(cfg)
+    log(f"weights generated in {time.perf_counter() - t0:.1f} s")
+    prompt = inputs.make_prompt(cfg)
+    model = binding.WiciModel(cfg, prefill_mode=args.prefill_mode,
+                              max_seq=cfg.prompt_len + n_decode)
+    t0 = time.perf_counter()
+    model.load_weights(w)
+    log(f"weights uploaded in {time.perf_counter() - t0:.1f} s")
+
+    for i in range(args.warmup):
+        ttft, dec, _ = run_request(model, prompt, n_decode)
+        log(f"warmup {i}: ttft {ttft * 1e3:.2f} ms, decode {n_decode / dec:.1f} tok/s")
+    torch.cuda.synchronize()
+    ttfts, decs = [], []
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        ttft, dec, tok = run_request(model, prompt, n_decode)
+        ttfts.append(ttft)
+        decs.append(dec)
+        log(f"step {i}: ttft {ttft * 1e3:.2f} ms, decode {n_decode / dec:.1f} tok/s")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+
+    decode_tok_s = n_decode * args.steps / sum(decs)
+    ttft_ms = float(np.median(ttfts)) * 1e3
+    mean_ctx = cfg.prompt_len + (n_decode + 1) / 2.0
+    bytes_tok = cfg.decode_bytes_per_token(int(round(mean_ctx)))
+    pf_flops = cfg.prefill_flops()
+    res = {
+        "metric": "batch-1 decode tokens/s (+ prefill TTFT ms, % of HBM roofline), 1 MI355X",
+        "value": decode_tok_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.weight_dtype, "data": "synthetic (seeded N(0,0.02^2) weights, uniform prompt ids)",
+        "config": {"workload": f"{cfg.name}-shaped dense decoder: {cfg.n_layers} layers, d {cfg.d_model}, "
+                               f"{cfg.n_heads}q/{cfg.n_kv_heads}kv heads x {cfg.head_dim}, FFN {cfg.ffn_dim}, "
+                               f"vocab {cfg.vocab}; prompt {cfg.prompt_len}, {n_decode} greedy decode steps, batch 1",
+                   "global_batch": 1, "seq_len": cfg.prompt_len + n_decode, "parallelism": "none"},
+        "ttft_ms": ttft_ms, "prefill_tok_s": cfg.prompt_len / (ttft_ms / 1e3),
+        "decode_bytes_per_token": bytes_tok,
+        "decode_hbm_frac": bytes_tok * decode_tok_s / HBM_PEAK,
+        "prefill_flops": pf_flops,
+        "prefill_mfma_frac": pf_flops / (ttft_ms / 1e3) / MFMA_BF16_PEAK,
+        "prefill_mode": args.prefill_mode or ("f32" if cfg.weight_dtype == "f32" else "bf16x2"),
+    }
+
+    if not args.no_profile:
+        log("profiling pass (eager launches, HIP events)")
+        mean, per_tok = profile_pass(model, cfg, prompt, n_decode)
+        gu = gateup_bytes(cfg)
+        ach = gu / (mean["gateup"] / 1e3)
+        res["roofline"] = {"kernel": "k_gemv gate/up (+RMSNorm prologue, SwiGLU epilogue)",
+                           "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9,
+                           "unit": "GB/s", "frac": ach / HBM_PEAK, "traffic": None,
+                           "bytes_per_launch": gu, "avg_launch_ms": mean["gateup"],
+                           "method": "HIP events around each launch, eager profiling pass over "
+                                     "one request's decode steps"}
+        res["decode_kernel_ms_per_token"] = per_tok
+        res["decode_kernel_sum_ms"] = float(sum(per_tok.values()))
+        res["decode_step_ms"] = 1e3 / decode_tok_s
+
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle sample)")
+        cb, (sp, sids, slogs) = cpu_baseline(cfg, w, args.cpu_prompt, args.cpu_decode)
+        # same sample through the GPU path
+        model.reset_kv()
+        g_ids, g_logs = model.generate(sp, args.cpu_decode, want_logits=True)
+        rel = max(float(np.max(np.abs(g - o)) / np.max(np.abs(o))) for g, o in zip(g_logs, slogs))
+        res["cpu_baseline"] = cb
+        res["parity_sample"] = {"ids_equal": [int(i) for i in g_ids] == [int(i) for i in sids],
+                                "max_rel_err": rel, "tokens": len(sids)}
+    model.close()
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,191 @@
+/*
+ * wici.h — C ABI of the offloaded decoder forward on one MI355X (gfx950).
+ *
+ * The paper moves an LLM application's GPU work to a remote GPU at the driver
+ * boundary: model tensors are uploaded tensor by tensor (Sec. "Model Caching"),
+ * and each generated token then runs one fixed group of GPU calls whose inputs
+ * follow from the token index (Sec. "Batching and Trace Replay", trace replay).
+ * Time to first token and the token rate are what the user sees (Sec.
+ * "Evaluation").  This header exposes exactly that work as four calls —
+ * wici_load_weights, wici_prefill, wici_decode_step, wici_reset_kv — plus the
+ * plumbing to create a model, size and bind its device memory, and read errors.
+ *
+ * What is computed: a dense pre-norm decoder-only transformer (RMSNorm, Q/K/V/O
+ * projections, rotate-half RoPE, causal grouped-query attention over a paged KV
+ * cache, SwiGLU MLP, final RMSNorm, LM head) and greedy argmax (lowest index
+ * among exactly equal maxima).
+ *
+ * Conventions for every call:
+ *  - Return codes only; nothing throws or aborts across this boundary.
+ *  - Arguments and state are checked before any GPU work is issued; a call that
+ *    fails a check changes nothing.
+ *  - A HIP runtime error returns WICI_E_HIP and puts the model in a sticky
+ *    failed state in which every call except wici_destroy / wici_last_error
+ *    returns WICI_E_STATE.
+ *  - A model is not thread-safe; use one model per thread (one client per
+ *    server thread, as in the paper's context management, Sec. "WiCi Library").
+ *  - Device memory is owned by the caller (see wici_bind_memory); the library
+ *    owns only host state, a captured decode graph and a 16-byte pinned host
+ *    staging buffer, all released by wici_destroy.
+ */
+#ifndef WICI_H
+#define WICI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct wici_model wici_model; /* opaque host-side model state */
+
+typedef enum {
+  WICI_OK = 0,
+  WICI_E_ARG = -1,      /* bad argument: pointer, size, token id, tensor name/shape/dtype */
+  WICI_E_STATE = -2,    /* call not allowed in the current state (or model failed) */
+  WICI_E_CAPACITY = -3, /* position + new tokens would exceed max_seq */
+  WICI_E_HIP = -4,      /* HIP runtime error; model is now failed */
+  WICI_E_NUMERIC = -5   /* a logit was NaN or infinite; no token is returned */
+} wici_status;
+
+typedef enum { WICI_F32 = 0, WICI_BF16 = 1 } wici_dtype;
+
+/* Arithmetic of the prefill projections (decode always multiplies bf16/fp32
+ * weights by fp32 activations with fp32 accumulation). */
+typedef enum {
+  WICI_PREFILL_BF16X2 = 0, /* MFMA bf16; fp32 activations split into hi+lo bf16
+                              terms (two products per tile): ~fp32-accurate */
+  WICI_PREFILL_BF16 = 1,   /* MFMA bf16; activations rounded to bf16 once */
+  WICI_PREFILL_F32 = 2     /* vector fp32 (required for fp32 weights) */
+} wici_prefill_mode;
+
+enum { WICI_FLAG_NO_GRAPH = 1 }; /* run decode steps eagerly instead of replaying a graph */
+
+typedef struct {
+  int32_t n_layers;
+  int32_t d_model;        /* multiple of 64 */
+  int32_t n_heads;        /* query heads, a multiple of n_kv_heads, n_heads/n_kv_heads <= 8 */
+  int32_t n_kv_heads;
+  int32_t head_dim;       /* 64 or 128 */
+  int32_t ffn_dim;        /* multiple of 64 */
+  int32_t vocab;          /* >= 1 */
+  float rms_eps;          /* > 0 */
+  double rope_base;       /* > 1 */
+  int32_t tied_embeddings;/* 1: the LM head is the embedding matrix */
+  int32_t weight_dtype;   /* wici_dtype of every matrix (norm gains are always F32) */
+  int32_t kv_dtype;       /* wici_dtype of the KV cache storage */
+  int32_t max_seq;        /* capacity in positions (prompt + generated) */
+  int32_t prefill_chunk;  /* prompt rows processed per pass; 1..8192 */
+  int32_t kv_page;        /* positions per KV page: 16, 32, 64 or 128 */
+  int32_t prefill_mode;   /* wici_prefill_mode; F32 is required when weight_dtype is F32 */
+  int32_t flags;          /* WICI_FLAG_* */
+} wici_config;
+
+/* One named weight tensor in logical [out, in] row-major layout.  Names:
+ *   tok_embeddings [vocab, d_model]
+ *   layers.<l>.attn_norm [d_model]           (F32)
+ *   layers.<l>.wq [n_heads*head_dim, d_model]
+ *   layers.<l>.wk, layers.<l>.wv [n_kv_heads*head_dim, d_model]
+ *   layers.<l>.wo [d_model, n_heads*head_dim]
+ *   layers.<l>.ffn_norm [d_model]            (F32)
+ *   layers.<l>.w_gate, layers.<l>.w_up [ffn_dim, d_model]
+ *   layers.<l>.w_down [d_model, ffn_dim]
+ *   norm [d_model]                           (F32)
+ *   lm_head [vocab, d_model]                 (absent when tied_embeddings)
+ * bf16 data is given as raw bf16 bit patterns (uint16). */
+typedef struct {
+  const char* name;
+  int32_t dtype;      /* wici_dtype */
+  int32_t ndim;       /* 1 or 2 */
+  int64_t shape[2];
+  const void* data;   /* host or device pointer (see on_device); borrowed for the call */
+  int32_t on_device;  /* 1: data is device memory on the model's GPU */
+} wici_tensor;
+
+/* Validate cfg and create host state.  hip_stream (hipStream_t, may be NULL for
+ * the null stream) is where every kernel of this model is launched; decode-step
+ * graph replay needs a non-NULL stream and is disabled on the null stream.
+ * Performs no GPU call.  Errors: WICI_E_ARG for a NULL pointer or an invalid or
+ * unsupported configuration. */
+wici_status wici_create(const wici_config* cfg, void* hip_stream, wici_model** out);
+
+/* Bytes of device memory the caller must provide for cfg (each region must be
+ * 256-byte aligned): packed weights, the paged KV cache, and scratch
+ * (activations, logits, reduction partials, device-side position and token).
+ * Performs no GPU call.  Errors: WICI_E_ARG. */
+wici_status wici_memory_requirements(const wici_config* cfg, size_t* weight_bytes,
+                                     size_t* kv_bytes, size_t* scratch_bytes);
+
+/* Bind caller-owned device memory (non-owning; it must outlive the model).
+ * Sizes must be at least those of wici_memory_requirements.  Allowed once, in
+ * the created state.  Also resets the KV cache state (position 0). */
+wici_status wici_bind_memory(wici_model* m, void* d_weights, size_t weight_bytes,
+                             void* d_kv, size_t kv_bytes, void* d_scratch,
+                             size_t scratch_bytes);
+
+/* Upload weight tensors (any subset, any order, any number of calls; a tensor
+ * given again overwrites the earlier copy).  The library repacks them into its
+ * fused device layout.  The model becomes ready once every required tensor has
+ * been given.  Synchronous.  Errors: WICI_E_ARG for an unknown, duplicate (within
+ * one call), mis-shaped or mis-typed tensor (nothing of that call is uploaded),
+ * WICI_E_STATE before wici_bind_memory. */
+wici_status wici_load_weights(wici_model* m, const wici_tensor* tensors, int32_t n_tensors);
+
+/* Append n_tokens prompt ids (host array) at the current position, processing
+ * them in chunks of prefill_chunk rows, and return the greedy next token (and,
+ * if logits is not NULL, the fp32 logits [vocab] of the last position into host
+ * memory).  Synchronous.  Errors: WICI_E_ARG (NULL tokens/first_token,
+ * n_tokens < 1, an id outside [0, vocab)), WICI_E_STATE (weights incomplete),
+ * WICI_E_CAPACITY (position + n_tokens > max_seq), WICI_E_NUMERIC (the
+ * positions were still appended; no token is returned, so a following decode
+ * step needs an explicit token_in). */
+wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
+                         int32_t* first_token, float* logits);
+
+/* One greedy decode step: feed token_in (or, when token_in < 0, the token the
+ * previous prefill/decode call returned) at the current position and return the
+ * next token (and optionally the logits, as for wici_prefill).  Synchronous.
+ * Errors: WICI_E_ARG (NULL next_token, token_in >= vocab), WICI_E_STATE (no
+ * prefill since the last reset), WICI_E_CAPACITY, WICI_E_NUMERIC. */
+wici_status wici_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
+                             float* logits);
+
+/* Forget the sequence: position 0, KV pages returned to the pool.  Weights stay. */
+wici_status wici_reset_kv(wici_model* m);
+
+/* Current position (number of cached positions).  Host state only. */
+wici_status wici_position(const wici_model* m, int32_t* pos);
+
+/* Diagnostic: copy the cached keys and values of one layer for positions
+ * [begin, end) into host arrays in logical layout [end-begin, n_kv_heads,
+ * head_dim] of the KV storage type (bf16 as uint16 bit patterns).  Synchronous.
+ * Errors: WICI_E_ARG for a bad layer or range (end must not exceed the current
+ * position), WICI_E_STATE before bind. */
+wici_status wici_read_kv(wici_model* m, int32_t layer, int32_t begin, int32_t end,
+                         void* host_k, void* host_v);
+
+/* Diagnostic: one decode step exactly as wici_decode_step (same arguments, checks
+ * and state effects) but launched eagerly, with a HIP event recorded on the
+ * model's stream around every kernel launch.  Writes the duration in ms of each
+ * launch, in launch order, to durations_ms (capacity entries) and their number
+ * (3 + 5 * n_layers) to *n_written.  Order: embedding; per layer: QKV GEMV,
+ * attention (split pass + merge), O GEMV, gate/up GEMV, down GEMV; then the LM
+ * head GEMV and the final argmax.  Errors as wici_decode_step, plus WICI_E_ARG
+ * for NULL outputs or a capacity below 3 + 5 * n_layers. */
+wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
+                                     float* durations_ms, int32_t capacity, int32_t* n_written);
+
+/* Message of the last failed call on this model ("" if none).  Valid until the
+ * next call on the model. */
+const char* wici_last_error(const wici_model* m);
+
+/* Free host state and the captured graph; NULL is allowed.  Device memory stays
+ * with the caller. */
+void wici_destroy(wici_model* m);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WICI_H */

@@ -167,9 +167,10 @@ class DecoderOracle:
     def _lm_weight(self) -> np.ndarray:
         return self.w["tok_embeddings"] if self.cfg.tied_embeddings else self.w["lm_head"]
 
-    def forward(self, tokens, all_logits: bool = False) -> np.ndarray:
+    def forward(self, tokens, all_logits: bool = False, first_row: int = 0) -> np.ndarray:
         """Append ``tokens`` at the current position; return the logits of the last
-        appended position ([vocab]) or of every appended position ([T, vocab])."""
+        appended position ([vocab]) or, with all_logits, of appended rows
+        first_row.. ([T - first_row, vocab])."""
         c = self.cfg
         tokens = np.asarray(tokens, dtype=np.int64).reshape(-1)
         T = tokens.size
@@ -199,7 +200,7 @@ class DecoderOracle:
             h = silu(wn @ self.w[pre + "w_gate"].T) * (wn @ self.w[pre + "w_up"].T)
             x = x + h @ self.w[pre + "w_down"].T
         self.pos = p0 + T
-        rows = x if all_logits else x[-1:]
+        rows = x[first_row:] if all_logits else x[-1:]
         logits = rms_norm(rows, self.w["norm"], c.rms_eps) @ self._lm_weight().T
         return logits if all_logits else logits[0]
 

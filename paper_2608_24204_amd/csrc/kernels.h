@@ -1,0 +1,77 @@
+// Host-side launchers of the libwici HIP kernels.  All pointers are device
+// pointers; every launcher enqueues on `st` and returns hipGetLastError().
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wici {
+
+enum GemvEpi { GEMV_STORE = 0, GEMV_RESID = 1, GEMV_SWIGLU = 2, GEMV_ARGMAX = 3 };
+
+struct ArgmaxPart { float v; int32_t i; };
+
+// y = W x for W [N, K] row-major (bf16 bits or fp32), x fp32 [K].
+// norm_gain != nullptr: x is first RMS-normalised (eps) and scaled by the gain.
+// STORE: y[n] = acc.  RESID: y[n] += acc.  SWIGLU: rows (2i, 2i+1) hold
+// (gate_i, up_i) and y[i] = silu(gate_i) * up_i.  ARGMAX: y[n] = acc and one
+// ArgmaxPart per block into `part` (grid size returned through *nblocks).
+hipError_t launch_gemv(bool w_bf16, int epi, const void* W, int N, int K, const float* x,
+                       const float* norm_gain, float eps, float* y, ArgmaxPart* part,
+                       int* nblocks, hipStream_t st);
+int gemv_argmax_blocks(int N);
+
+// Final argmax over `n` partials -> st->token; st->pos += advance (or = set_pos
+// when set_pos >= 0); st->bad set when a partial carries index -1 (a logit was
+// not finite), in which case st->token = -1.
+hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int advance,
+                               int set_pos, hipStream_t st);
+
+// x[t, :] = E[tokens[t], :] for t < T (tokens == nullptr: the state's token, T = 1).
+hipError_t launch_embed(bool w_bf16, const void* E, int d, const int32_t* tokens, int T,
+                        const void* state, float* x, hipStream_t st);
+hipError_t launch_set_token(void* state, int token, hipStream_t st);
+hipError_t launch_reset_state(void* state, hipStream_t st);
+hipError_t launch_init_block_table(int32_t* table, int n_pages, hipStream_t st);
+
+// y[t, :] = RMSNorm(x[t, :]) * gain for T rows of width d.
+hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int T, int d,
+                               float* y, hipStream_t st);
+
+struct KvLayout {
+  void* base;            // this layer's pool
+  const int32_t* table;  // logical page -> physical page
+  int page;              // positions per page
+  int n_kv;              // KV heads
+  int hd;                // head dim
+  // element offset of (phys page, kv 0/1, head h, slot s, dim d):
+  //   ((phys * 2 + kv) * n_kv + h) * page * hd + s * hd + d
+};
+
+// Prefill: rotate q (in place) and k of T rows at positions p0..p0+T-1 and
+// append k, v to the cache.  qkv rows are [Hq*hd | Hkv*hd | Hkv*hd] fp32.
+hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
+                              const float* cos_t, const float* sin_t, KvLayout kv,
+                              hipStream_t st);
+
+// Prefill attention: queries = rotated q rows of qkv (T rows at p0..), keys =
+// cache positions [0, p0+T), causal; out [T, Hq*hd] fp32.
+hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
+                               KvLayout kv, float* out, hipStream_t st);
+
+// Decode attention at position state->pos: rotates q and the new k, appends the
+// new k, v, attends over [0, pos] in nsplit splits, then combines into out
+// [Hq*hd] fp32.
+hipError_t launch_attn_decode(bool kv_bf16, const float* qkv, int Hq, const float* cos_t,
+                              const float* sin_t, KvLayout kv, const void* state,
+                              int nsplit, float* part_o, float* part_ml, float* out,
+                              hipStream_t st);
+
+// C[M, N] (ldc) = A[M, K] (fp32, lda) x W[N, K]^T with epilogue as launch_gemv
+// (STORE / RESID / SWIGLU; SWIGLU writes C[M, N/2]).
+//   mode 0: MFMA bf16, A split into hi + lo bf16 terms
+//   mode 1: MFMA bf16, A rounded to bf16
+//   mode 2: vector fp32 (W bf16 or fp32)
+hipError_t launch_gemm(int mode, bool w_bf16, int epi, const float* A, int lda, const void* W,
+                       int M, int N, int K, float* C, int ldc, hipStream_t st);
+
+}  // namespace wici

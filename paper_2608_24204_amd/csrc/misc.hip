@@ -1,0 +1,193 @@
+// Small memory-bound kernels of the forward: embedding gather, row RMSNorm,
+// RoPE + KV-cache append for prefill rows, the second argmax pass and the
+// device-side step state.
+#include "common.h"
+#include "kernels.h"
+
+namespace wici {
+
+// ---- embedding ------------------------------------------------------------------
+template <typename WT>
+__global__ __launch_bounds__(256) void k_embed(const WT* __restrict__ E, int d,
+                                               const int32_t* __restrict__ tokens,
+                                               const DecodeState* __restrict__ st,
+                                               float* __restrict__ x) {
+  const int t = blockIdx.x;
+  const int tok = tokens ? tokens[t] : st->token;
+  const WT* row = E + (size_t)tok * d;
+  for (int k = threadIdx.x * 8; k < d; k += 256 * 8) {
+    float v[8];
+    load8(row + k, v);
+    float4* o = reinterpret_cast<float4*>(x + (size_t)t * d + k);
+    o[0] = make_float4(v[0], v[1], v[2], v[3]);
+    o[1] = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+hipError_t launch_embed(bool w_bf16, const void* E, int d, const int32_t* tokens, int T,
+                        const void* state, float* x, hipStream_t st) {
+  const DecodeState* s = static_cast<const DecodeState*>(state);
+  if (w_bf16)
+    hipLaunchKernelGGL(k_embed<bf16_t>, dim3(T), dim3(256), 0, st,
+                       static_cast<const bf16_t*>(E), d, tokens, s, x);
+  else
+    hipLaunchKernelGGL(k_embed<float>, dim3(T), dim3(256), 0, st,
+                       static_cast<const float*>(E), d, tokens, s, x);
+  return hipGetLastError();
+}
+
+__global__ void k_set_token(DecodeState* st, int token) { st->token = token; }
+
+__global__ void k_reset_state(DecodeState* st) {
+  st->pos = 0;
+  st->token = 0;
+  st->bad = 0;
+  st->pad = 0;
+}
+
+hipError_t launch_reset_state(void* state, hipStream_t st) {
+  hipLaunchKernelGGL(k_reset_state, dim3(1), dim3(1), 0, st, static_cast<DecodeState*>(state));
+  return hipGetLastError();
+}
+
+hipError_t launch_set_token(void* state, int token, hipStream_t st) {
+  hipLaunchKernelGGL(k_set_token, dim3(1), dim3(1), 0, st, static_cast<DecodeState*>(state),
+                     token);
+  return hipGetLastError();
+}
+
+// Pages are handed out from the top of the pool down, so logical page i lives in
+// physical page n_pages-1-i: any kernel that ignored the table would read the
+// wrong page.
+__global__ void k_init_block_table(int32_t* table, int n_pages) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_pages) table[i] = n_pages - 1 - i;
+}
+
+hipError_t launch_init_block_table(int32_t* table, int n_pages, hipStream_t st) {
+  hipLaunchKernelGGL(k_init_block_table, dim3((n_pages + 255) / 256), dim3(256), 0, st, table,
+                     n_pages);
+  return hipGetLastError();
+}
+
+// ---- RMSNorm of T rows ------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_rmsnorm_rows(const float* __restrict__ x,
+                                                      const float* __restrict__ g, float eps,
+                                                      int d, float* __restrict__ y) {
+  __shared__ float red[4];
+  const float* xr = x + (size_t)blockIdx.x * d;
+  float* yr = y + (size_t)blockIdx.x * d;
+  float ss = 0.f;
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + k);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  const float r = 1.0f / sqrtf(block256_sum(ss, red) / (float)d + eps);
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    float4 v = *reinterpret_cast<const float4*>(xr + k);
+    const float4 w = *reinterpret_cast<const float4*>(g + k);
+    v.x = v.x * r * w.x; v.y = v.y * r * w.y; v.z = v.z * r * w.z; v.w = v.w * r * w.w;
+    *reinterpret_cast<float4*>(yr + k) = v;
+  }
+}
+
+hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int T, int d,
+                               float* y, hipStream_t st) {
+  hipLaunchKernelGGL(k_rmsnorm_rows, dim3(T), dim3(256), 0, st, x, gain, eps, d, y);
+  return hipGetLastError();
+}
+
+// ---- RoPE + KV append for prefill rows --------------------------------------------
+// One block per row; thread j < hd/2 of a head rotates the pair (j, j + hd/2).
+template <typename KT>
+__global__ __launch_bounds__(256) void k_rope_append(float* __restrict__ qkv, int p0, int Hq,
+                                                     const float* __restrict__ cos_t,
+                                                     const float* __restrict__ sin_t,
+                                                     KvLayout kv) {
+  const int t = blockIdx.x, pos = p0 + t;
+  const int hd = kv.hd, half = hd >> 1, Hkv = kv.n_kv;
+  const int width = (Hq + 2 * Hkv) * hd;
+  float* row = qkv + (size_t)t * width;
+  const float* cr = cos_t + (size_t)pos * half;
+  const float* sr = sin_t + (size_t)pos * half;
+  KT* base = static_cast<KT*>(kv.base);
+  const int phys = kv.table[pos / kv.page], slot = pos % kv.page;
+  // rotate q heads in place, k heads into the cache
+  for (int i = threadIdx.x; i < (Hq + Hkv) * half; i += blockDim.x) {
+    const int h = i / half, j = i % half;
+    float* z = row + h * hd;
+    const float a = z[j], b = z[j + half], c = cr[j], s = sr[j];
+    const float ra = a * c - b * s, rb = a * s + b * c;
+    if (h < Hq) {
+      z[j] = ra;
+      z[j + half] = rb;
+    } else {
+      const int g = h - Hq;
+      KT* dst = base + (((size_t)phys * 2 + 0) * Hkv + g) * kv.page * hd + (size_t)slot * hd;
+      Elem<KT>::store(dst + j, ra);
+      Elem<KT>::store(dst + j + half, rb);
+    }
+  }
+  for (int i = threadIdx.x; i < Hkv * hd; i += blockDim.x) {
+    const int g = i / hd, e = i % hd;
+    KT* dst = base + (((size_t)phys * 2 + 1) * Hkv + g) * kv.page * hd + (size_t)slot * hd;
+    Elem<KT>::store(dst + e, row[(Hq + Hkv) * hd + i]);
+  }
+}
+
+hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
+                              const float* cos_t, const float* sin_t, KvLayout kv,
+                              hipStream_t st) {
+  if (kv_bf16)
+    hipLaunchKernelGGL(k_rope_append<bf16_t>, dim3(T), dim3(256), 0, st, qkv, p0, Hq, cos_t,
+                       sin_t, kv);
+  else
+    hipLaunchKernelGGL(k_rope_append<float>, dim3(T), dim3(256), 0, st, qkv, p0, Hq, cos_t,
+                       sin_t, kv);
+  return hipGetLastError();
+}
+
+// ---- argmax, second pass -------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restrict__ part,
+                                                        int n, DecodeState* st, int advance,
+                                                        int set_pos) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
+  __shared__ int sbad[16];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  int bad = 0;
+  for (int i = tid; i < n; i += 1024) {
+    const ArgmaxPart p = part[i];
+    if (p.i < 0) bad = 1;
+    else if (am_better(p.v, p.i, bv, bi)) { bv = p.v; bi = p.i; }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(bv, m);
+    const int oi = __shfl_xor(bi, m);
+    if (am_better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    bad |= __shfl_xor(bad, m);
+  }
+  if (lane == 0) { sv[w] = bv; si[w] = bi; sbad[w] = bad; }
+  __syncthreads();
+  if (tid == 0) {
+    for (int k = 1; k < 16; ++k) {
+      if (am_better(sv[k], si[k], bv, bi)) { bv = sv[k]; bi = si[k]; }
+      bad |= sbad[k];
+    }
+    st->bad = bad;
+    st->token = bad ? -1 : bi;
+    st->pos = set_pos >= 0 ? set_pos : st->pos + advance;
+  }
+}
+
+hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int advance,
+                               int set_pos, hipStream_t st) {
+  hipLaunchKernelGGL(k_argmax_final, dim3(1), dim3(1024), 0, st, part, n,
+                     static_cast<DecodeState*>(state), advance, set_pos);
+  return hipGetLastError();
+}
+
+}  // namespace wici

@@ -1,0 +1,618 @@
+// libwici runtime and C ABI: configuration checks, device memory layout, weight
+// packing, the chunked-prefill loop, and the per-token decode step, captured
+// once as a HIP graph and replayed for every token (the fixed per-token call
+// group the paper replays as a trace, Sec. "Batching and Trace Replay").
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "../../include/wici.h"
+#include "common.h"
+#include "kernels.h"
+
+using wici::ArgmaxPart;
+using wici::DecodeState;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kMaxGemvBlocks = 1024;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+size_t dsize(int32_t dt) { return dt == WICI_BF16 ? 2 : 4; }
+
+struct Layout {
+  // weights
+  size_t l_wqkv, l_wo, l_wgu, l_wdown, l_anorm, l_fnorm, layer_stride;
+  size_t embed, final_norm, lm_head, rope_cos, rope_sin, weight_bytes;
+  // kv
+  int n_pages;
+  size_t kv_layer_stride, kv_bytes;
+  // scratch
+  size_t x, a, qkv, att, h, logits, parts, part_o, part_ml, tokens, table, state, scratch_bytes;
+  int nsplit;
+};
+
+bool config_ok(const wici_config* c, std::string* why) {
+  auto bad = [&](const char* m) { if (why) *why = m; return false; };
+  if (!c) return bad("config is NULL");
+  if (c->n_layers < 1 || c->n_layers > 4096) return bad("n_layers out of range");
+  if (c->d_model < 64 || c->d_model % 64) return bad("d_model must be a positive multiple of 64");
+  if (c->ffn_dim < 64 || c->ffn_dim % 64) return bad("ffn_dim must be a positive multiple of 64");
+  if (c->head_dim != 64 && c->head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (c->n_kv_heads < 1 || c->n_heads < 1 || c->n_heads % c->n_kv_heads)
+    return bad("n_heads must be a positive multiple of n_kv_heads");
+  if (c->n_heads / c->n_kv_heads > 8) return bad("at most 8 query heads per KV head");
+  if (c->vocab < 1) return bad("vocab must be >= 1");
+  if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return bad("rms_eps must be > 0");
+  if (!(c->rope_base > 1.0) || !std::isfinite(c->rope_base)) return bad("rope_base must be > 1");
+  if (c->weight_dtype != WICI_F32 && c->weight_dtype != WICI_BF16) return bad("bad weight_dtype");
+  if (c->kv_dtype != WICI_F32 && c->kv_dtype != WICI_BF16) return bad("bad kv_dtype");
+  if (c->max_seq < 1 || c->max_seq > (1 << 20)) return bad("max_seq out of range");
+  if (c->prefill_chunk < 1 || c->prefill_chunk > 8192) return bad("prefill_chunk out of range");
+  if (c->kv_page != 16 && c->kv_page != 32 && c->kv_page != 64 && c->kv_page != 128)
+    return bad("kv_page must be 16, 32, 64 or 128");
+  if (c->prefill_mode < WICI_PREFILL_BF16X2 || c->prefill_mode > WICI_PREFILL_F32)
+    return bad("bad prefill_mode");
+  if (c->weight_dtype == WICI_F32 && c->prefill_mode != WICI_PREFILL_F32)
+    return bad("fp32 weights need prefill_mode WICI_PREFILL_F32");
+  if (c->flags & ~WICI_FLAG_NO_GRAPH) return bad("unknown flags");
+  if (c->tied_embeddings != 0 && c->tied_embeddings != 1) return bad("tied_embeddings must be 0 or 1");
+  return true;
+}
+
+Layout make_layout(const wici_config& c) {
+  Layout L{};
+  const size_t ws = dsize(c.weight_dtype), d = c.d_model, F = c.ffn_dim, V = c.vocab;
+  const size_t qd = (size_t)c.n_heads * c.head_dim, kvd = (size_t)c.n_kv_heads * c.head_dim;
+  const size_t nqkv = qd + 2 * kvd;
+  size_t o = 0;
+  L.l_wqkv = o; o = align_up(o + nqkv * d * ws);
+  L.l_wo = o; o = align_up(o + d * qd * ws);
+  L.l_wgu = o; o = align_up(o + 2 * F * d * ws);
+  L.l_wdown = o; o = align_up(o + d * F * ws);
+  L.l_anorm = o; o = align_up(o + d * 4);
+  L.l_fnorm = o; o = align_up(o + d * 4);
+  L.layer_stride = o;
+  o = L.layer_stride * c.n_layers;
+  L.embed = o; o = align_up(o + V * d * ws);
+  L.final_norm = o; o = align_up(o + d * 4);
+  if (c.tied_embeddings) {
+    L.lm_head = L.embed;
+  } else {
+    L.lm_head = o; o = align_up(o + V * d * ws);
+  }
+  const size_t half = c.head_dim / 2;
+  L.rope_cos = o; o = align_up(o + (size_t)c.max_seq * half * 4);
+  L.rope_sin = o; o = align_up(o + (size_t)c.max_seq * half * 4);
+  L.weight_bytes = o;
+
+  L.n_pages = (c.max_seq + c.kv_page - 1) / c.kv_page;
+  L.kv_layer_stride = align_up((size_t)L.n_pages * 2 * c.n_kv_heads * c.kv_page * c.head_dim *
+                               dsize(c.kv_dtype));
+  L.kv_bytes = L.kv_layer_stride * c.n_layers;
+
+  L.nsplit = std::max(32, (c.max_seq + 255) / 256);
+  const size_t C = c.prefill_chunk;
+  o = 0;
+  L.x = o; o = align_up(o + C * d * 4);
+  L.a = o; o = align_up(o + C * d * 4);
+  L.qkv = o; o = align_up(o + C * nqkv * 4);
+  L.att = o; o = align_up(o + C * qd * 4);
+  L.h = o; o = align_up(o + C * F * 4);
+  L.logits = o; o = align_up(o + V * 4);
+  L.parts = o; o = align_up(o + kMaxGemvBlocks * sizeof(ArgmaxPart));
+  L.part_o = o; o = align_up(o + (size_t)c.n_heads * L.nsplit * c.head_dim * 4);
+  L.part_ml = o; o = align_up(o + (size_t)c.n_heads * L.nsplit * 2 * 4);
+  L.tokens = o; o = align_up(o + C * 4);
+  L.table = o; o = align_up(o + (size_t)L.n_pages * 4);
+  L.state = o; o = align_up(o + sizeof(DecodeState));
+  L.scratch_bytes = o;
+  return L;
+}
+
+enum TensorKind { T_EMBED, T_FINAL_NORM, T_LM_HEAD, T_ANORM, T_WQ, T_WK, T_WV, T_WO, T_FNORM,
+                  T_GATE, T_UP, T_DOWN };
+
+struct TensorSpec {
+  TensorKind kind;
+  int layer;
+  int32_t dtype;
+  int ndim;
+  int64_t rows, cols;
+};
+
+}  // namespace
+
+struct wici_model {
+  wici_config cfg{};
+  Layout L{};
+  hipStream_t stream = nullptr;
+  bool bound = false, failed = false;
+  char* dw = nullptr;
+  char* dkv = nullptr;
+  char* ds = nullptr;
+  std::string err;
+  std::unordered_map<std::string, int> spec_index;
+  std::vector<TensorSpec> specs;
+  std::vector<uint8_t> loaded;
+  int n_loaded = 0;
+  int32_t pos = 0;
+  bool have_token = false;
+  DecodeState* h_state = nullptr;  // pinned staging
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t gexec = nullptr;
+  int gemv_lm_blocks = 0;
+
+  bool ready() const { return bound && n_loaded == (int)specs.size(); }
+  template <typename T> T* W(size_t off) const { return reinterpret_cast<T*>(dw + off); }
+  template <typename T> T* S(size_t off) const { return reinterpret_cast<T*>(ds + off); }
+  size_t layer(int l, size_t off) const { return (size_t)l * L.layer_stride + off; }
+  wici::KvLayout kv(int l) const {
+    wici::KvLayout k;
+    k.base = dkv + (size_t)l * L.kv_layer_stride;
+    k.table = S<int32_t>(L.table);
+    k.page = cfg.kv_page;
+    k.n_kv = cfg.n_kv_heads;
+    k.hd = cfg.head_dim;
+    return k;
+  }
+};
+
+namespace {
+
+wici_status fail(wici_model* m, wici_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  m->err = buf;
+  return s;
+}
+
+#define HIP_TRY(m, expr)                                                                   \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) {                                                                \
+      (m)->failed = true;                                                                  \
+      return fail((m), WICI_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));         \
+    }                                                                                      \
+  } while (0)
+
+void build_specs(wici_model* m) {
+  const wici_config& c = m->cfg;
+  const int64_t d = c.d_model, F = c.ffn_dim, V = c.vocab;
+  const int64_t qd = (int64_t)c.n_heads * c.head_dim, kvd = (int64_t)c.n_kv_heads * c.head_dim;
+  auto add = [&](const std::string& name, TensorKind k, int l, int32_t dt, int nd, int64_t r,
+                 int64_t cc) {
+    m->spec_index[name] = (int)m->specs.size();
+    m->specs.push_back({k, l, dt, nd, r, cc});
+  };
+  const int32_t wd = c.weight_dtype;
+  add("tok_embeddings", T_EMBED, -1, wd, 2, V, d);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const std::string p = "layers." + std::to_string(l) + ".";
+    add(p + "attn_norm", T_ANORM, l, WICI_F32, 1, d, 1);
+    add(p + "wq", T_WQ, l, wd, 2, qd, d);
+    add(p + "wk", T_WK, l, wd, 2, kvd, d);
+    add(p + "wv", T_WV, l, wd, 2, kvd, d);
+    add(p + "wo", T_WO, l, wd, 2, d, qd);
+    add(p + "ffn_norm", T_FNORM, l, WICI_F32, 1, d, 1);
+    add(p + "w_gate", T_GATE, l, wd, 2, F, d);
+    add(p + "w_up", T_UP, l, wd, 2, F, d);
+    add(p + "w_down", T_DOWN, l, wd, 2, d, F);
+  }
+  add("norm", T_FINAL_NORM, -1, WICI_F32, 1, d, 1);
+  if (!c.tied_embeddings) add("lm_head", T_LM_HEAD, -1, wd, 2, V, d);
+  m->loaded.assign(m->specs.size(), 0);
+}
+
+bool usable(const wici_model* m) { return m && !m->failed; }
+
+// Enqueue one decode step (position and input token read from device state).
+// With `marks`, an event is recorded before the first launch and after every
+// launcher call (the profiling entry point uses this; graph capture never does).
+hipError_t enqueue_decode(wici_model* m, std::vector<hipEvent_t>* marks = nullptr) {
+  const wici_config& c = m->cfg;
+  const Layout& L = m->L;
+  const bool wb = c.weight_dtype == WICI_BF16, kb = c.kv_dtype == WICI_BF16;
+  const int d = c.d_model, F = c.ffn_dim, qd = c.n_heads * c.head_dim;
+  const int nqkv = qd + 2 * c.n_kv_heads * c.head_dim;
+  float* x = m->S<float>(L.x);
+  float* qkv = m->S<float>(L.qkv);
+  float* att = m->S<float>(L.att);
+  float* h = m->S<float>(L.h);
+  void* st = m->ds + L.state;
+  hipStream_t s = m->stream;
+  hipError_t e;
+  auto mark = [&]() -> hipError_t {
+    if (!marks) return hipSuccess;
+    hipEvent_t ev;
+    hipError_t r = hipEventCreate(&ev);
+    if (r != hipSuccess) return r;
+    marks->push_back(ev);
+    return hipEventRecord(ev, s);
+  };
+#define WICI_STEP(call) \
+  do {                  \
+    if ((e = (call))) return e; \
+    if ((e = mark())) return e; \
+  } while (0)
+  if ((e = mark())) return e;
+  WICI_STEP(wici::launch_embed(wb, m->dw + L.embed, d, nullptr, 1, st, x, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    WICI_STEP(wici::launch_gemv(wb, wici::GEMV_STORE, m->dw + m->layer(l, L.l_wqkv), nqkv, d, x,
+                                m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, qkv, nullptr,
+                                nullptr, s));
+    WICI_STEP(wici::launch_attn_decode(kb, qkv, c.n_heads, m->W<float>(L.rope_cos),
+                                       m->W<float>(L.rope_sin), m->kv(l), st, L.nsplit,
+                                       m->S<float>(L.part_o), m->S<float>(L.part_ml), att, s));
+    WICI_STEP(wici::launch_gemv(wb, wici::GEMV_RESID, m->dw + m->layer(l, L.l_wo), d, qd, att,
+                                nullptr, 0.f, x, nullptr, nullptr, s));
+    WICI_STEP(wici::launch_gemv(wb, wici::GEMV_SWIGLU, m->dw + m->layer(l, L.l_wgu), 2 * F, d, x,
+                                m->W<float>(m->layer(l, L.l_fnorm)), c.rms_eps, h, nullptr,
+                                nullptr, s));
+    WICI_STEP(wici::launch_gemv(wb, wici::GEMV_RESID, m->dw + m->layer(l, L.l_wdown), d, F, h,
+                                nullptr, 0.f, x, nullptr, nullptr, s));
+  }
+  int nb = 0;
+  WICI_STEP(wici::launch_gemv(wb, wici::GEMV_ARGMAX, m->dw + L.lm_head, c.vocab, d, x,
+                              m->W<float>(L.final_norm), c.rms_eps, m->S<float>(L.logits),
+                              m->S<ArgmaxPart>(L.parts), &nb, s));
+  WICI_STEP(wici::launch_argmax_final(m->S<ArgmaxPart>(L.parts), nb, st, 1, -1, s));
+#undef WICI_STEP
+  return hipSuccess;
+}
+
+// Enqueue one prefill chunk of T rows at positions p0.. (token ids already on
+// the device); x[T-1] holds the last row's residual stream afterwards.
+hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
+  const wici_config& c = m->cfg;
+  const Layout& L = m->L;
+  const bool wb = c.weight_dtype == WICI_BF16, kb = c.kv_dtype == WICI_BF16;
+  const int d = c.d_model, F = c.ffn_dim, qd = c.n_heads * c.head_dim;
+  const int nqkv = qd + 2 * c.n_kv_heads * c.head_dim;
+  const int mode = c.prefill_mode;
+  float* x = m->S<float>(L.x);
+  float* a = m->S<float>(L.a);
+  float* qkv = m->S<float>(L.qkv);
+  float* att = m->S<float>(L.att);
+  float* h = m->S<float>(L.h);
+  hipStream_t s = m->stream;
+  hipError_t e;
+  if ((e = wici::launch_embed(wb, m->dw + L.embed, d, m->S<int32_t>(L.tokens), T, nullptr, x, s)))
+    return e;
+  for (int l = 0; l < c.n_layers; ++l) {
+    if ((e = wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, T, d,
+                                       a, s)))
+      return e;
+    if ((e = wici::launch_gemm(mode, wb, wici::GEMV_STORE, a, d, m->dw + m->layer(l, L.l_wqkv), T,
+                               nqkv, d, qkv, nqkv, s)))
+      return e;
+    if ((e = wici::launch_rope_append(kb, qkv, T, p0, c.n_heads, m->W<float>(L.rope_cos),
+                                      m->W<float>(L.rope_sin), m->kv(l), s)))
+      return e;
+    if ((e = wici::launch_attn_prefill(kb, qkv, T, p0, c.n_heads, m->kv(l), att, s))) return e;
+    if ((e = wici::launch_gemm(mode, wb, wici::GEMV_RESID, att, qd, m->dw + m->layer(l, L.l_wo), T,
+                               d, qd, x, d, s)))
+      return e;
+    if ((e = wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_fnorm)), c.rms_eps, T, d,
+                                       a, s)))
+      return e;
+    if ((e = wici::launch_gemm(mode, wb, wici::GEMV_SWIGLU, a, d, m->dw + m->layer(l, L.l_wgu), T,
+                               2 * F, d, h, F, s)))
+      return e;
+    if ((e = wici::launch_gemm(mode, wb, wici::GEMV_RESID, h, F, m->dw + m->layer(l, L.l_wdown), T,
+                               d, F, x, d, s)))
+      return e;
+  }
+  return hipSuccess;
+}
+
+wici_status finish_step(wici_model* m, int32_t* tok, float* logits) {
+  HIP_TRY(m, hipMemcpyAsync(m->h_state, m->ds + m->L.state, sizeof(DecodeState),
+                            hipMemcpyDeviceToHost, m->stream));
+  if (logits)
+    HIP_TRY(m, hipMemcpyAsync(logits, m->ds + m->L.logits, (size_t)m->cfg.vocab * 4,
+                              hipMemcpyDeviceToHost, m->stream));
+  HIP_TRY(m, hipStreamSynchronize(m->stream));
+  m->pos = m->h_state->pos;
+  if (m->h_state->bad) {
+    m->have_token = false;
+    return fail(m, WICI_E_NUMERIC, "non-finite logits at position %d", m->pos - 1);
+  }
+  *tok = m->h_state->token;
+  m->have_token = true;
+  return WICI_OK;
+}
+
+}  // namespace
+
+// ============================================================================ C ABI
+
+extern "C" {
+
+wici_status wici_memory_requirements(const wici_config* cfg, size_t* weight_bytes,
+                                     size_t* kv_bytes, size_t* scratch_bytes) {
+  if (!config_ok(cfg, nullptr) || !weight_bytes || !kv_bytes || !scratch_bytes) return WICI_E_ARG;
+  const Layout L = make_layout(*cfg);
+  *weight_bytes = L.weight_bytes;
+  *kv_bytes = L.kv_bytes;
+  *scratch_bytes = L.scratch_bytes;
+  return WICI_OK;
+}
+
+wici_status wici_create(const wici_config* cfg, void* hip_stream, wici_model** out) {
+  if (!out) return WICI_E_ARG;
+  *out = nullptr;
+  if (!config_ok(cfg, nullptr)) return WICI_E_ARG;
+  wici_model* m = new (std::nothrow) wici_model();
+  if (!m) return WICI_E_ARG;
+  m->cfg = *cfg;
+  m->L = make_layout(*cfg);
+  m->stream = static_cast<hipStream_t>(hip_stream);
+  build_specs(m);
+  *out = m;
+  return WICI_OK;
+}
+
+wici_status wici_bind_memory(wici_model* m, void* d_weights, size_t weight_bytes, void* d_kv,
+                             size_t kv_bytes, void* d_scratch, size_t scratch_bytes) {
+  if (!m) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (m->bound) return fail(m, WICI_E_STATE, "memory already bound");
+  if (!d_weights || !d_kv || !d_scratch) return fail(m, WICI_E_ARG, "NULL device pointer");
+  if (weight_bytes < m->L.weight_bytes || kv_bytes < m->L.kv_bytes ||
+      scratch_bytes < m->L.scratch_bytes)
+    return fail(m, WICI_E_ARG, "device region too small");
+  if (((uintptr_t)d_weights | (uintptr_t)d_kv | (uintptr_t)d_scratch) % kAlign)
+    return fail(m, WICI_E_ARG, "device regions must be 256-byte aligned");
+  m->dw = static_cast<char*>(d_weights);
+  m->dkv = static_cast<char*>(d_kv);
+  m->ds = static_cast<char*>(d_scratch);
+  HIP_TRY(m, hipHostMalloc((void**)&m->h_state, sizeof(DecodeState), hipHostMallocDefault));
+  // RoPE angle table: pos * base^(-2j/hd), evaluated in double, stored as fp32.
+  const wici_config& c = m->cfg;
+  const int half = c.head_dim / 2;
+  std::vector<float> cs((size_t)c.max_seq * half), sn((size_t)c.max_seq * half);
+  for (int j = 0; j < half; ++j) {
+    const double inv = std::pow(c.rope_base, -2.0 * j / c.head_dim);
+    for (int p = 0; p < c.max_seq; ++p) {
+      const double ang = (double)p * inv;
+      cs[(size_t)p * half + j] = (float)std::cos(ang);
+      sn[(size_t)p * half + j] = (float)std::sin(ang);
+    }
+  }
+  HIP_TRY(m, hipMemcpy(m->dw + m->L.rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(m, hipMemcpy(m->dw + m->L.rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(m, wici::launch_init_block_table(m->S<int32_t>(m->L.table), m->L.n_pages, m->stream));
+  HIP_TRY(m, wici::launch_reset_state(m->ds + m->L.state, m->stream));
+  HIP_TRY(m, hipStreamSynchronize(m->stream));
+  m->bound = true;
+  m->pos = 0;
+  m->have_token = false;
+  return WICI_OK;
+}
+
+wici_status wici_load_weights(wici_model* m, const wici_tensor* tensors, int32_t n_tensors) {
+  if (!m) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (!m->bound) return fail(m, WICI_E_STATE, "wici_bind_memory must come first");
+  if (n_tensors < 0 || (n_tensors > 0 && !tensors)) return fail(m, WICI_E_ARG, "bad tensor list");
+  std::vector<int> idx(n_tensors);
+  std::vector<uint8_t> seen(m->specs.size(), 0);
+  for (int i = 0; i < n_tensors; ++i) {
+    const wici_tensor& t = tensors[i];
+    if (!t.name) return fail(m, WICI_E_ARG, "tensor %d has no name", i);
+    auto it = m->spec_index.find(t.name);
+    if (it == m->spec_index.end()) return fail(m, WICI_E_ARG, "unknown tensor '%s'", t.name);
+    const TensorSpec& sp = m->specs[it->second];
+    if (seen[it->second]) return fail(m, WICI_E_ARG, "tensor '%s' given twice", t.name);
+    seen[it->second] = 1;
+    if (t.dtype != sp.dtype) return fail(m, WICI_E_ARG, "tensor '%s': wrong dtype", t.name);
+    const bool shape_ok = sp.ndim == 1 ? (t.ndim == 1 && t.shape[0] == sp.rows)
+                                       : (t.ndim == 2 && t.shape[0] == sp.rows && t.shape[1] == sp.cols);
+    if (!shape_ok) return fail(m, WICI_E_ARG, "tensor '%s': wrong shape", t.name);
+    if (!t.data) return fail(m, WICI_E_ARG, "tensor '%s': NULL data", t.name);
+    idx[i] = it->second;
+  }
+  const wici_config& c = m->cfg;
+  const Layout& L = m->L;
+  const size_t ws = dsize(c.weight_dtype), d = c.d_model;
+  const size_t qd = (size_t)c.n_heads * c.head_dim, kvd = (size_t)c.n_kv_heads * c.head_dim;
+  for (int i = 0; i < n_tensors; ++i) {
+    const wici_tensor& t = tensors[i];
+    const TensorSpec& sp = m->specs[idx[i]];
+    const hipMemcpyKind kind = t.on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    const size_t es = dsize(sp.dtype);
+    const size_t bytes = (size_t)sp.rows * sp.cols * es;
+    char* dst = nullptr;
+    switch (sp.kind) {
+      case T_EMBED: dst = m->dw + L.embed; break;
+      case T_FINAL_NORM: dst = m->dw + L.final_norm; break;
+      case T_LM_HEAD: dst = m->dw + L.lm_head; break;
+      case T_ANORM: dst = m->dw + m->layer(sp.layer, L.l_anorm); break;
+      case T_FNORM: dst = m->dw + m->layer(sp.layer, L.l_fnorm); break;
+      case T_WQ: dst = m->dw + m->layer(sp.layer, L.l_wqkv); break;
+      case T_WK: dst = m->dw + m->layer(sp.layer, L.l_wqkv) + qd * d * ws; break;
+      case T_WV: dst = m->dw + m->layer(sp.layer, L.l_wqkv) + (qd + kvd) * d * ws; break;
+      case T_WO: dst = m->dw + m->layer(sp.layer, L.l_wo); break;
+      case T_DOWN: dst = m->dw + m->layer(sp.layer, L.l_wdown); break;
+      case T_GATE:
+      case T_UP: {
+        // gate row i -> packed row 2i, up row i -> packed row 2i+1
+        const size_t rb = d * ws;
+        char* base = m->dw + m->layer(sp.layer, L.l_wgu) + (sp.kind == T_UP ? rb : 0);
+        HIP_TRY(m, hipMemcpy2DAsync(base, 2 * rb, t.data, rb, rb, (size_t)sp.rows, kind, m->stream));
+        continue;
+      }
+    }
+    HIP_TRY(m, hipMemcpyAsync(dst, t.data, bytes, kind, m->stream));
+  }
+  HIP_TRY(m, hipStreamSynchronize(m->stream));
+  for (int i = 0; i < n_tensors; ++i)
+    if (!m->loaded[idx[i]]) { m->loaded[idx[i]] = 1; ++m->n_loaded; }
+  return WICI_OK;
+}
+
+wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
+                         int32_t* first_token, float* logits) {
+  if (!m) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (!tokens || !first_token) return fail(m, WICI_E_ARG, "NULL tokens or first_token");
+  if (n_tokens < 1) return fail(m, WICI_E_ARG, "n_tokens must be >= 1");
+  for (int i = 0; i < n_tokens; ++i)
+    if (tokens[i] < 0 || tokens[i] >= m->cfg.vocab)
+      return fail(m, WICI_E_ARG, "token id %d at %d outside [0, %d)", tokens[i], i, m->cfg.vocab);
+  if (!m->ready()) return fail(m, WICI_E_STATE, "weights not bound/loaded");
+  if ((int64_t)m->pos + n_tokens > m->cfg.max_seq)
+    return fail(m, WICI_E_CAPACITY, "position %d + %d tokens exceeds max_seq %d", m->pos, n_tokens,
+                m->cfg.max_seq);
+  const wici_config& c = m->cfg;
+  const Layout& L = m->L;
+  const int C = c.prefill_chunk;
+  int last_T = 0;
+  for (int c0 = 0; c0 < n_tokens; c0 += C) {
+    const int T = std::min(C, n_tokens - c0);
+    HIP_TRY(m, hipMemcpyAsync(m->ds + L.tokens, tokens + c0, (size_t)T * 4, hipMemcpyHostToDevice,
+                              m->stream));
+    HIP_TRY(m, enqueue_prefill_chunk(m, m->pos + c0, T));
+    // the token buffer is reused by the next chunk: wait for this one
+    if (c0 + C < n_tokens) HIP_TRY(m, hipStreamSynchronize(m->stream));
+    last_T = T;
+  }
+  int nb = 0;
+  const bool wb = c.weight_dtype == WICI_BF16;
+  HIP_TRY(m, wici::launch_gemv(wb, wici::GEMV_ARGMAX, m->dw + L.lm_head, c.vocab, c.d_model,
+                               m->S<float>(L.x) + (size_t)(last_T - 1) * c.d_model,
+                               m->W<float>(L.final_norm), c.rms_eps, m->S<float>(L.logits),
+                               m->S<ArgmaxPart>(L.parts), &nb, m->stream));
+  HIP_TRY(m, wici::launch_argmax_final(m->S<ArgmaxPart>(L.parts), nb, m->ds + L.state, 0,
+                                       m->pos + n_tokens, m->stream));
+  return finish_step(m, first_token, logits);
+}
+
+wici_status wici_decode_step(wici_model* m, int32_t token_in, int32_t* next_token, float* logits) {
+  if (!m) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (!next_token) return fail(m, WICI_E_ARG, "NULL next_token");
+  if (token_in >= m->cfg.vocab) return fail(m, WICI_E_ARG, "token id %d >= vocab", token_in);
+  if (!m->ready()) return fail(m, WICI_E_STATE, "weights not bound/loaded");
+  if (m->pos < 1) return fail(m, WICI_E_STATE, "decode before prefill");
+  if (token_in < 0 && !m->have_token) return fail(m, WICI_E_STATE, "no previous token to feed");
+  if (m->pos + 1 > m->cfg.max_seq)
+    return fail(m, WICI_E_CAPACITY, "position %d reached max_seq", m->pos);
+  if (token_in >= 0) HIP_TRY(m, wici::launch_set_token(m->ds + m->L.state, token_in, m->stream));
+  const bool use_graph = m->stream != nullptr && !(m->cfg.flags & WICI_FLAG_NO_GRAPH);
+  if (use_graph) {
+    if (!m->gexec) {
+      HIP_TRY(m, hipStreamBeginCapture(m->stream, hipStreamCaptureModeThreadLocal));
+      const hipError_t e = enqueue_decode(m);
+      hipGraph_t g = nullptr;
+      const hipError_t e2 = hipStreamEndCapture(m->stream, &g);
+      HIP_TRY(m, e);
+      HIP_TRY(m, e2);
+      m->graph = g;
+      HIP_TRY(m, hipGraphInstantiate(&m->gexec, m->graph, nullptr, nullptr, 0));
+    }
+    HIP_TRY(m, hipGraphLaunch(m->gexec, m->stream));
+  } else {
+    HIP_TRY(m, enqueue_decode(m));
+  }
+  return finish_step(m, next_token, logits);
+}
+
+wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
+                                     float* durations_ms, int32_t capacity, int32_t* n_written) {
+  if (!m) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (!next_token || !durations_ms || !n_written) return fail(m, WICI_E_ARG, "NULL output");
+  const int need = 3 + 5 * m->cfg.n_layers;
+  if (capacity < need) return fail(m, WICI_E_ARG, "capacity %d < %d launches", capacity, need);
+  if (token_in >= m->cfg.vocab) return fail(m, WICI_E_ARG, "token id %d >= vocab", token_in);
+  if (!m->ready()) return fail(m, WICI_E_STATE, "weights not bound/loaded");
+  if (m->pos < 1) return fail(m, WICI_E_STATE, "decode before prefill");
+  if (token_in < 0 && !m->have_token) return fail(m, WICI_E_STATE, "no previous token to feed");
+  if (m->pos + 1 > m->cfg.max_seq)
+    return fail(m, WICI_E_CAPACITY, "position %d reached max_seq", m->pos);
+  if (token_in >= 0) HIP_TRY(m, wici::launch_set_token(m->ds + m->L.state, token_in, m->stream));
+  std::vector<hipEvent_t> ev;
+  const hipError_t e = enqueue_decode(m, &ev);
+  const hipError_t e2 = e == hipSuccess ? hipStreamSynchronize(m->stream) : e;
+  int n = 0;
+  if (e2 == hipSuccess)
+    for (size_t i = 1; i < ev.size(); ++i) {
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, ev[i - 1], ev[i]) == hipSuccess) durations_ms[n] = ms;
+      ++n;
+    }
+  for (hipEvent_t x : ev) (void)hipEventDestroy(x);
+  HIP_TRY(m, e2);
+  *n_written = n;
+  return finish_step(m, next_token, nullptr);
+}
+
+wici_status wici_reset_kv(wici_model* m) {
+  if (!m) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (!m->bound) return fail(m, WICI_E_STATE, "memory not bound");
+  HIP_TRY(m, wici::launch_init_block_table(m->S<int32_t>(m->L.table), m->L.n_pages, m->stream));
+  HIP_TRY(m, wici::launch_reset_state(m->ds + m->L.state, m->stream));
+  HIP_TRY(m, hipStreamSynchronize(m->stream));
+  m->pos = 0;
+  m->have_token = false;
+  return WICI_OK;
+}
+
+wici_status wici_position(const wici_model* m, int32_t* pos) {
+  if (!m || !pos) return WICI_E_ARG;
+  *pos = m->pos;
+  return WICI_OK;
+}
+
+wici_status wici_read_kv(wici_model* m, int32_t layer, int32_t begin, int32_t end, void* host_k,
+                         void* host_v) {
+  if (!m) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (!m->bound) return fail(m, WICI_E_STATE, "memory not bound");
+  const wici_config& c = m->cfg;
+  if (layer < 0 || layer >= c.n_layers || begin < 0 || end < begin || end > m->pos || !host_k ||
+      !host_v)
+    return fail(m, WICI_E_ARG, "bad layer/range/pointer");
+  const size_t es = dsize(c.kv_dtype), hd = c.head_dim, page = c.kv_page, nkv = c.n_kv_heads;
+  std::vector<int32_t> table(m->L.n_pages);
+  HIP_TRY(m, hipMemcpyAsync(table.data(), m->ds + m->L.table, table.size() * 4,
+                            hipMemcpyDeviceToHost, m->stream));
+  HIP_TRY(m, hipStreamSynchronize(m->stream));
+  const char* base = m->dkv + (size_t)layer * m->L.kv_layer_stride;
+  for (int p = begin; p < end; ++p) {
+    const size_t phys = table[p / page], slot = p % page;
+    for (int w = 0; w < 2; ++w) {
+      const char* src = base + (((phys * 2 + w) * nkv) * page + slot) * hd * es;
+      char* dst = static_cast<char*>(w ? host_v : host_k) + (size_t)(p - begin) * nkv * hd * es;
+      HIP_TRY(m, hipMemcpy2DAsync(dst, hd * es, src, page * hd * es, hd * es, nkv,
+                                  hipMemcpyDeviceToHost, m->stream));
+    }
+  }
+  HIP_TRY(m, hipStreamSynchronize(m->stream));
+  return WICI_OK;
+}
+
+const char* wici_last_error(const wici_model* m) { return m ? m->err.c_str() : "NULL model"; }
+
+void wici_destroy(wici_model* m) {
+  if (!m) return;
+  if (m->gexec) (void)hipGraphExecDestroy(m->gexec);
+  if (m->graph) (void)hipGraphDestroy(m->graph);
+  if (m->h_state) (void)hipHostFree(m->h_state);
+  delete m;
+}
+
+}  // extern "C"

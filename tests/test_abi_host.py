@@ -1,0 +1,118 @@
+"""The C-ABI library without a GPU: it loads, exports every declared entry point,
+and its host-side checks (configuration, arguments, state) return the documented
+status codes before any GPU call is made."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_24204_amd import binding, configs
+from tests.helpers import small_cfg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.skipif(not os.path.exists(binding.LIB_PATH),
+                                reason="libwici.so not built")
+
+
+def test_every_declared_symbol_is_exported():
+    lib = binding.load_library()
+    header = open(os.path.join(ROOT, "include", "wici.h")).read()
+    declared = set(re.findall(r"\b(wici_[a-z_]+)\s*\(", header))
+    assert declared == set(binding.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def _cfg(**kw):
+    return binding.make_config(small_cfg(d_model=256, n_heads=4, n_kv_heads=2, head_dim=64,
+                                         ffn_dim=512, vocab=1000, **kw))
+
+
+@pytest.mark.parametrize("name", list(configs.CONFIGS))
+def test_memory_requirements_cover_the_weights(name):
+    cfg = configs.CONFIGS[name]
+    w, kv, s = binding.memory_requirements(binding.make_config(cfg))
+    assert w >= cfg.n_params() * cfg.wbytes
+    assert w < cfg.n_params() * cfg.wbytes * 1.01 + (64 << 20)
+    per_pos = cfg.n_layers * 2 * cfg.kv_dim * cfg.kvbytes
+    assert kv >= cfg.max_seq * per_pos
+    assert all(v % 256 == 0 for v in (w, kv, s))
+
+
+@pytest.mark.parametrize("field,value", [
+    ("head_dim", 96), ("d_model", 100), ("ffn_dim", 96 + 1), ("n_kv_heads", 3),
+    ("n_layers", 0), ("vocab", 0), ("kv_page", 48), ("prefill_chunk", 0),
+    ("max_seq", 0), ("rms_eps", 0.0), ("rope_base", 1.0), ("prefill_mode", 7),
+    ("flags", 8), ("weight_dtype", 5), ("tied_embeddings", 2)])
+def test_invalid_config_is_rejected(field, value):
+    lib = binding.load_library()
+    c = _cfg()
+    setattr(c, field, value)
+    h = ctypes.c_void_p()
+    assert lib.wici_create(ctypes.byref(c), None, ctypes.byref(h)) == binding.WICI_E_ARG
+    assert not h.value
+    sz = ctypes.c_size_t()
+    assert lib.wici_memory_requirements(ctypes.byref(c), ctypes.byref(sz), ctypes.byref(sz),
+                                        ctypes.byref(sz)) == binding.WICI_E_ARG
+
+
+def test_group_limit_and_fp32_weights_need_fp32_prefill():
+    lib = binding.load_library()
+    h = ctypes.c_void_p()
+    c = _cfg(); c.n_heads, c.n_kv_heads = 18, 2
+    assert lib.wici_create(ctypes.byref(c), None, ctypes.byref(h)) == binding.WICI_E_ARG
+    c = _cfg(); c.weight_dtype = binding.WICI_F32; c.prefill_mode = binding.PREFILL_MODES["bf16x2"]
+    assert lib.wici_create(ctypes.byref(c), None, ctypes.byref(h)) == binding.WICI_E_ARG
+
+
+def test_state_machine_before_memory_is_bound():
+    lib = binding.load_library()
+    c = _cfg()
+    h = ctypes.c_void_p()
+    assert lib.wici_create(ctypes.byref(c), None, ctypes.byref(h)) == binding.WICI_OK
+    try:
+        pos = ctypes.c_int32(-1)
+        assert lib.wici_position(h, ctypes.byref(pos)) == binding.WICI_OK and pos.value == 0
+        assert lib.wici_load_weights(h, None, 0) == binding.WICI_E_STATE
+        assert b"bind" in lib.wici_last_error(h)
+        toks = (ctypes.c_int32 * 3)(1, 2, 3)
+        out = ctypes.c_int32()
+        # argument checks come first ...
+        assert lib.wici_prefill(h, toks, 0, ctypes.byref(out), None) == binding.WICI_E_ARG
+        bad = (ctypes.c_int32 * 2)(1, 1000)
+        assert lib.wici_prefill(h, bad, 2, ctypes.byref(out), None) == binding.WICI_E_ARG
+        assert lib.wici_prefill(h, toks, 3, None, None) == binding.WICI_E_ARG
+        # ... then the state checks
+        assert lib.wici_prefill(h, toks, 3, ctypes.byref(out), None) == binding.WICI_E_STATE
+        assert lib.wici_decode_step(h, -1, ctypes.byref(out), None) == binding.WICI_E_STATE
+        assert lib.wici_decode_step(h, 1000, ctypes.byref(out), None) == binding.WICI_E_ARG
+        assert lib.wici_reset_kv(h) == binding.WICI_E_STATE
+        buf = (ctypes.c_uint16 * 64)()
+        assert lib.wici_read_kv(h, 0, 0, 1, buf, buf) == binding.WICI_E_STATE
+        assert lib.wici_bind_memory(h, None, 0, None, 0, None, 0) == binding.WICI_E_ARG
+        # a region that is too small is refused before anything is touched
+        w, k, s = binding.memory_requirements(c)
+        fake = ctypes.c_void_p(1 << 20)
+        assert lib.wici_bind_memory(h, fake, w - 256, fake, k, fake, s) == binding.WICI_E_ARG
+        misaligned = ctypes.c_void_p((1 << 20) + 8)
+        assert lib.wici_bind_memory(h, misaligned, w, fake, k, fake, s) == binding.WICI_E_ARG
+        assert lib.wici_position(h, None) == binding.WICI_E_ARG
+    finally:
+        lib.wici_destroy(h)
+    lib.wici_destroy(None)
+    assert lib.wici_create(ctypes.byref(c), None, None) == binding.WICI_E_ARG
+    assert lib.wici_create(None, None, ctypes.byref(h)) == binding.WICI_E_ARG
+
+
+def test_tensor_array_marshalling():
+    import numpy as np
+    cfg = small_cfg(d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn_dim=512, vocab=100,
+                    weight_dtype="bf16", kv_dtype="bf16")
+    w = {"tok_embeddings": np.zeros((100, 256), np.uint16), "norm": np.ones(256, np.float32)}
+    arr, keep = binding.tensor_array(cfg, w)
+    assert arr[0].name == b"tok_embeddings" and arr[0].dtype == binding.WICI_BF16
+    assert arr[0].ndim == 2 and tuple(arr[0].shape) == (100, 256) and arr[0].on_device == 0
+    assert arr[1].dtype == binding.WICI_F32 and arr[1].ndim == 1 and arr[1].shape[0] == 256

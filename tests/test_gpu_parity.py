@@ -1,0 +1,222 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on the
+same seeded inputs.  Tolerances: logits max relative error (infinity norm) 1e-4
+for fp32 weights, 2e-2 for bf16 weights; greedy ids identical at every step."""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_24204_amd import configs, inputs
+from tests.parity import compare, oracle_step_logits
+
+pytestmark = pytest.mark.gpu
+
+_W = {}
+
+
+def weights_for(cfg, gain_std=0.0):
+    key = (cfg, gain_std)
+    if key not in _W:
+        w = inputs.make_weights(cfg, gain_std=gain_std)
+        _W.clear()  # keep at most one large weight set alive
+        _W[key] = (w, inputs.weights_f64(cfg, w))
+    return _W[key]
+
+
+def make_model(cfg, w, **kw):
+    from paper_2608_24204_amd.binding import WiciModel
+    m = WiciModel(cfg, **kw)
+    m.load_weights(w)
+    return m
+
+
+def tol_for(cfg):
+    return 1e-4 if cfg.weight_dtype == "f32" else 2e-2
+
+
+def run_parity(cfg, prompt, n_steps, gain_std=0.0, **kw):
+    w, w64 = weights_for(cfg, gain_std)
+    m = make_model(cfg, w, **kw)
+    try:
+        ids, logs = m.generate(prompt, n_steps, want_logits=True)
+    finally:
+        m.close()
+    ora = oracle_step_logits(cfg, w64, prompt, ids)
+    rep = compare(ids, logs, ora)
+    print(f"[parity] {cfg.name} P={len(prompt)} N={n_steps} {kw} -> {rep.summary()}", flush=True)
+    return rep, ids, logs
+
+
+# ---- small shapes exercising every kernel path --------------------------------------
+
+SMALL = {
+    "mha64_f32": configs.ModelConfig(name="t_mha64", key=70, n_layers=2, d_model=256, n_heads=4,
+                                     n_kv_heads=4, head_dim=64, ffn_dim=512, vocab=1000,
+                                     weight_dtype="f32", kv_dtype="f32", prompt_len=40,
+                                     decode_steps=12),
+    "gqa64_bf16": configs.ModelConfig(name="t_gqa64", key=71, n_layers=2, d_model=512, n_heads=8,
+                                      n_kv_heads=2, head_dim=64, ffn_dim=1024, vocab=3001,
+                                      prompt_len=77, decode_steps=12, tied_embeddings=True,
+                                      rope_base=500000.0),
+    "gqa128_bf16": configs.ModelConfig(name="t_gqa128", key=72, n_layers=2, d_model=512,
+                                       n_heads=8, n_kv_heads=2, head_dim=128, ffn_dim=768,
+                                       vocab=2500, prompt_len=150, decode_steps=12),
+    "g5_bf16": configs.ModelConfig(name="t_g5", key=73, n_layers=1, d_model=640, n_heads=10,
+                                   n_kv_heads=2, head_dim=128, ffn_dim=1536, vocab=1531,
+                                   prompt_len=33, decode_steps=8, rope_base=1e6),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_configs_match_oracle(cuda_ok, name):
+    cfg = SMALL[name]
+    prompt = inputs.make_prompt(cfg)
+    rep, _, _ = run_parity(cfg, prompt, cfg.decode_steps, gain_std=0.1, kv_page=16)
+    assert rep.max_rel_err <= tol_for(cfg)
+    assert rep.strict_ids, rep.summary()
+
+
+def test_tiny_config(cuda_ok):
+    cfg = configs.TINY
+    rep, _, _ = run_parity(cfg, inputs.make_prompt(cfg), cfg.decode_steps)
+    assert rep.max_rel_err <= 1e-4
+    assert rep.strict_ids, rep.summary()
+
+
+@pytest.mark.parametrize("P,chunk,page", [(1, 64, 16), (63, 64, 16), (65, 64, 32),
+                                          (200, 64, 16), (129, 128, 128), (300, 2048, 64)])
+def test_ragged_prompts_chunks_and_pages(cuda_ok, P, chunk, page):
+    cfg = SMALL["gqa128_bf16"]
+    prompt = inputs.make_prompt(cfg, P)
+    rep, _, _ = run_parity(cfg, prompt, 20, gain_std=0.1, prefill_chunk=chunk, kv_page=page,
+                           max_seq=P + 21)
+    assert rep.max_rel_err <= 2e-2
+    assert rep.strict_ids, rep.summary()
+
+
+@pytest.mark.parametrize("mode", ["bf16x2", "bf16", "f32"])
+def test_prefill_modes(cuda_ok, mode):
+    cfg = SMALL["gqa64_bf16"]
+    prompt = inputs.make_prompt(cfg, 130)
+    rep, _, _ = run_parity(cfg, prompt, 4, gain_std=0.1, prefill_mode=mode, max_seq=140)
+    assert rep.max_rel_err <= 2e-2
+    if mode != "bf16":
+        assert rep.max_rel_err <= 1e-3
+        assert rep.strict_ids, rep.summary()
+
+
+def test_kv_cache_holds_oracle_values(cuda_ok):
+    cfg = SMALL["gqa128_bf16"]
+    w, w64 = weights_for(cfg, 0.1)
+    prompt = inputs.make_prompt(cfg, 70)
+    m = make_model(cfg, w, kv_page=16, prefill_chunk=32, max_seq=80)
+    try:
+        tok, _ = m.prefill(prompt)
+        m.decode_step(-1)
+        m.decode_step(-1)
+        K, V = m.read_kv(1, 0, 72)
+    finally:
+        m.close()
+    orc = oracle.DecoderOracle(cfg, w64, max_seq=80)
+    orc.prefill(prompt)
+    orc.decode(tok)
+    # the third position's input is the GPU's second token; only positions < 72 compared
+    ok = orc.K[1][:71]
+    gk = inputs.bf16_bits_to_f32(K[:71]).astype(np.float64)
+    gv = inputs.bf16_bits_to_f32(V[:71]).astype(np.float64)
+    for g, o in ((gk, ok), (gv, orc.V[1][:71])):
+        ulp = np.abs(o) * 2.0 ** -7 + 1e-30
+        assert np.all(np.abs(g - o) <= ulp)          # at most one bf16 step apart
+        assert np.mean(g != o) < 0.01                # and almost always identical
+
+
+def test_graph_replay_equals_eager_and_is_deterministic(cuda_ok):
+    cfg = SMALL["gqa64_bf16"]
+    w, _ = weights_for(cfg, 0.1)
+    prompt = inputs.make_prompt(cfg, 50)
+    out = []
+    for graph in (True, False, True):
+        m = make_model(cfg, w, graph=graph, max_seq=70)
+        try:
+            out.append(m.generate(prompt, 10, want_logits=True))
+        finally:
+            m.close()
+    (i0, l0), (i1, l1), (i2, l2) = out
+    assert i0 == i1 == i2
+    for a, b, c in zip(l0, l1, l2):
+        assert np.array_equal(a, b) and np.array_equal(a, c)
+
+
+def test_split_prefill_equals_joint_prefill(cuda_ok):
+    cfg = SMALL["gqa128_bf16"]
+    w, _ = weights_for(cfg, 0.1)
+    prompt = inputs.make_prompt(cfg, 90)
+    m = make_model(cfg, w, max_seq=100)
+    try:
+        t_joint, l_joint = m.prefill(prompt, True)
+        m.reset_kv()
+        assert m.position == 0
+        m.prefill(prompt[:37])
+        t_split, l_split = m.prefill(prompt[37:], True)
+        assert m.position == 90
+    finally:
+        m.close()
+    assert t_joint == t_split
+    assert np.max(np.abs(l_joint - l_split)) / np.max(np.abs(l_joint)) < 1e-4
+
+
+def test_errors_and_state(cuda_ok):
+    from paper_2608_24204_amd.binding import WiciError, WICI_E_ARG, WICI_E_CAPACITY, WICI_E_STATE
+    cfg = SMALL["gqa64_bf16"]
+    w, _ = weights_for(cfg, 0.1)
+    m = make_model(cfg, w, max_seq=20)
+    try:
+        with pytest.raises(WiciError) as e:
+            m.decode_step(-1)
+        assert e.value.status == WICI_E_STATE
+        with pytest.raises(WiciError) as e:
+            m.prefill(np.zeros(21, np.int32))
+        assert e.value.status == WICI_E_CAPACITY
+        with pytest.raises(WiciError) as e:
+            m.prefill([0, cfg.vocab])
+        assert e.value.status == WICI_E_ARG
+        assert m.position == 0
+        m.prefill(np.arange(19) % cfg.vocab)
+        tok, _ = m.decode_step(5)
+        assert 0 <= tok < cfg.vocab and m.position == 20
+        with pytest.raises(WiciError) as e:
+            m.decode_step(-1)
+        assert e.value.status == WICI_E_CAPACITY
+        m.reset_kv()
+        with pytest.raises(WiciError) as e:
+            m.decode_step(-1)
+        assert e.value.status == WICI_E_STATE
+        t2, _ = m.prefill(np.arange(19) % cfg.vocab)
+        assert 0 <= t2 < cfg.vocab
+    finally:
+        m.close()
+
+
+def test_non_finite_logits_are_reported(cuda_ok):
+    from paper_2608_24204_amd.binding import WiciError, WICI_E_NUMERIC, WICI_E_STATE
+    cfg = SMALL["mha64_f32"]
+    w, _ = weights_for(cfg, 0.1)
+    w = dict(w)
+    lm = w["lm_head"].copy()
+    lm[17, 3] = np.nan
+    w["lm_head"] = lm
+    m = make_model(cfg, w, max_seq=20)
+    try:
+        with pytest.raises(WiciError) as e:
+            m.prefill([1, 2, 3])
+        assert e.value.status == WICI_E_NUMERIC
+        with pytest.raises(WiciError) as e:
+            m.decode_step(-1)          # no token to feed back
+        assert e.value.status == WICI_E_STATE
+        with pytest.raises(WiciError) as e:
+            m.decode_step(4)           # an explicit token runs, and fails again
+        assert e.value.status == WICI_E_NUMERIC
+    finally:
+        m.close()
