@@ -115,21 +115,32 @@ def test_kv_cache_holds_oracle_values(cuda_ok):
     try:
         tok, _ = m.prefill(prompt)
         m.decode_step(-1)
-        m.decode_step(-1)
-        K, V = m.read_kv(1, 0, 72)
+        kv = [m.read_kv(l, 0, 71) for l in range(cfg.n_layers)]
     finally:
         m.close()
     orc = oracle.DecoderOracle(cfg, w64, max_seq=80)
     orc.prefill(prompt)
     orc.decode(tok)
-    # the third position's input is the GPU's second token; only positions < 72 compared
-    ok = orc.K[1][:71]
-    gk = inputs.bf16_bits_to_f32(K[:71]).astype(np.float64)
-    gv = inputs.bf16_bits_to_f32(V[:71]).astype(np.float64)
-    for g, o in ((gk, ok), (gv, orc.V[1][:71])):
-        ulp = np.abs(o) * 2.0 ** -7 + 1e-30
-        assert np.all(np.abs(g - o) <= ulp)          # at most one bf16 step apart
-        assert np.mean(g != o) < 0.01                # and almost always identical
+    for l, (K, V) in enumerate(kv):
+        for bits, o in ((K, orc.K[l][:71]), (V, orc.V[l][:71])):
+            g = inputs.bf16_bits_to_f32(bits).astype(np.float64)
+            assert np.array_equal(g, oracle.bf16_round(g))   # stored as bf16 values
+            scale = np.max(np.abs(o))
+            if l == 0:
+                # layer 0 sees exact inputs: both sides round a value they computed
+                # to bf16 and the GPU's value carries only float32 rounding, so the
+                # results are at most one bf16 step apart (near zero: within the
+                # float32 error of the value itself), and almost always identical
+                bound = np.abs(o) * 2.0 ** -7 + scale * 2.0 ** -16
+                viol = np.abs(g - o) > bound
+                assert not viol.any(), (np.argwhere(viol)[:5], g[viol][:5], o[viol][:5])
+                assert np.mean(g != o) < 0.01
+            else:
+                # deeper layers also carry the one-step differences of the cache
+                # below them through attention: compare at the logit tolerance scale
+                # (one storage step plus the propagated error)
+                assert np.all(np.abs(g - o) <= np.abs(o) * 2.0 ** -7 + 2e-3 * scale)
+                assert np.mean(g != o) < 0.2
 
 
 def test_graph_replay_equals_eager_and_is_deterministic(cuda_ok):
