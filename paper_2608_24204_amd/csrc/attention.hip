@@ -1,12 +1,11 @@
 // Causal grouped-query attention over the paged KV cache.
 //
-// Decode (one query position per head): split-K over the context.  Grid =
-// (nsplit, n_kv_heads); a block loads each cached key/value of its range once and
-// serves all query heads of the KV head's group with it (GQA), so every cached
-// byte is read once per step.  The new position's k/v are rotated, rounded to the
-// storage type, written to the cache and used straight from LDS (no block reads a
-// position another block of the same launch writes).  A second tiny kernel merges
-// the splits with their (max, sum) statistics.
+// Decode (one query position per head): split-K over the context.  A block loads
+// each cached key/value of its range once and serves all query heads of the KV
+// head's group with it (GQA), so every cached byte is read once per step.  The
+// new position's k/v are rotated, rounded to the storage type, written to the
+// cache and used straight from LDS (no block reads a position another block of
+// the same launch writes).  A second small kernel merges the splits.
 //
 // Prefill: one block per (64 queries, query head), keys streamed through LDS in
 // blocks of 64 with an online softmax, fp32 throughout.
@@ -16,7 +15,6 @@
 namespace wici {
 
 constexpr int kMaxGroup = 8;   // query heads per KV head
-constexpr int kMaxChunk = 256; // positions per decode split
 
 __device__ __forceinline__ size_t kv_off(const KvLayout& kv, int pos, int which, int h) {
   const int phys = kv.table[pos / kv.page], slot = pos % kv.page;
@@ -24,46 +22,70 @@ __device__ __forceinline__ size_t kv_off(const KvLayout& kv, int pos, int which,
 }
 
 // ------------------------------------------------------------------- decode
-template <int HD, typename KT>
+// Grid (nsplit, Hkv): block (s, g) owns positions [64 s, 64 s + 64) of KV head g;
+// blocks past the current context exit at once, so one captured launch serves
+// every position.  The block's page-table entries are read before the position
+// is known and all of its cached keys and values are requested before the query
+// is rotated.  Each block writes its unnormalised output and (max, sum)
+// statistics; a second kernel merges the splits.  (Merging in the last block of
+// each head would need device-scope fences, whose L2 write-back and invalidate
+// on every block cost more than the extra launch.)
+constexpr int kChunk = 64;       // positions per decode split
+constexpr int kMaxSplits = 256;  // splits the merge kernel holds in LDS
+
+template <int HD, typename KT, int G>
 __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ qkv, int Hq,
                                                      const float* __restrict__ cos_t,
                                                      const float* __restrict__ sin_t,
                                                      KvLayout kv,
                                                      const DecodeState* __restrict__ st,
-                                                     int nsplit, float* __restrict__ part_o,
+                                                     float* __restrict__ part_o,
                                                      float* __restrict__ part_ml) {
-  constexpr int LPP = HD / 8;   // lanes per position (8 elements each)
-  constexpr int PPW = 64 / LPP; // positions per wave per pass
-  constexpr int PPB = 4 * PPW;  // positions per block per pass
+  constexpr int LPP = HD / 8;       // lanes per position (8 elements each)
+  constexpr int PPW = 64 / LPP;     // positions per wave per pass
+  constexpr int PPB = 4 * PPW;      // positions per block per pass
+  constexpr int NP = kChunk / PPB;  // passes over the chunk
   constexpr int HALF = HD / 2;
-  __shared__ float qs[kMaxGroup][HD];
-  __shared__ float sc[kMaxGroup][kMaxChunk];
+  __shared__ float qs[G][HD];
+  __shared__ float sc[G][kChunk];
   __shared__ float knew[HD], vnew[HD];
-  __shared__ float accs[4][kMaxGroup][HD];
-  __shared__ float mls[kMaxGroup][2];
+  __shared__ float accs[4][G][HD];
+  __shared__ float mls[G][2];
 
+  const int nsplit = gridDim.x;
   const int split = blockIdx.x, g = blockIdx.y;
-  const int Hkv = kv.n_kv, G = Hq / Hkv;
+  const int Hkv = kv.n_kv;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int pg = lane / LPP, sub = lane % LPP;
+  const int start = split * kChunk;
+  // page of each of this lane's positions (independent of the current position)
+  int phys[NP];
+#pragma unroll
+  for (int i = 0; i < NP; ++i) {
+    const int j = start + i * PPB + wave * PPW + pg;
+    phys[i] = kv.table[min(j, kv.max_pos - 1) / kv.page];
+  }
   const int pos = st->pos, n = pos + 1;
-  const int chunk = (n + nsplit - 1) / nsplit;
-  const int start = split * chunk, end = min(n, start + chunk);
+  if (start >= n) return;
+  const int end = min(n, start + kChunk);
   const KT* base = static_cast<const KT*>(kv.base);
+  const size_t head_stride = (size_t)kv.page * HD;
+  auto addr = [&](int p, int j, int which) {
+    return base + (((size_t)p * 2 + which) * Hkv + g) * head_stride + (size_t)(j % kv.page) * HD;
+  };
 
-  if (start >= end) {  // empty split: contributes nothing to the merge
-    for (int i = tid; i < G * HD; i += 256) {
-      const int h = g * G + i / HD;
-      part_o[((size_t)h * nsplit + split) * HD + i % HD] = 0.f;
+  // ---- request every cached key/value of the chunk --------------------------------
+  float kr[NP][8], vr[NP][8];
+#pragma unroll
+  for (int i = 0; i < NP; ++i) {
+    const int j = start + i * PPB + wave * PPW + pg;
+    if (j < end && j != pos) {
+      load8(addr(phys[i], j, 0) + sub * 8, kr[i]);
+      load8(addr(phys[i], j, 1) + sub * 8, vr[i]);
     }
-    if (tid < G) {
-      const int h = g * G + tid;
-      part_ml[((size_t)h * nsplit + split) * 2 + 0] = -INFINITY;
-      part_ml[((size_t)h * nsplit + split) * 2 + 1] = 0.f;
-    }
-    return;
   }
 
-  // rotated, pre-scaled queries of the group
+  // ---- rotated, pre-scaled queries; the new position's key/value ------------------
   const float scale = 1.0f / sqrtf((float)HD);
   const float* cr = cos_t + (size_t)pos * HALF;
   const float* sr = sin_t + (size_t)pos * HALF;
@@ -74,12 +96,12 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
     qs[h][j] = (a * c - b * s) * scale;
     qs[h][j + HALF] = (a * s + b * c) * scale;
   }
-  const bool has_new = end == n;
-  if (has_new) {
+  if (end == n) {  // this split holds the new position: rotate, round, append
     const float* kz = qkv + (size_t)Hq * HD + (size_t)g * HD;
     const float* vz = kz + (size_t)Hkv * HD;
-    KT* kd = const_cast<KT*>(base) + kv_off(kv, pos, 0, g);
-    KT* vd = const_cast<KT*>(base) + kv_off(kv, pos, 1, g);
+    const int pp = kv.table[pos / kv.page];
+    KT* kd = const_cast<KT*>(addr(pp, pos, 0));
+    KT* vd = const_cast<KT*>(addr(pp, pos, 1));
     for (int j = tid; j < HALF; j += 256) {
       const float a = kz[j], b = kz[j + HALF], c = cr[j], s = sr[j];
       const float ra = Elem<KT>::round(a * c - b * s), rb = Elem<KT>::round(a * s + b * c);
@@ -96,95 +118,92 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
   }
   __syncthreads();
 
-  const int pg = lane / LPP, sub = lane % LPP;
-  float qr[kMaxGroup][8];
+  // ---- scores ------------------------------------------------------------------------
+  float q[G][8];
 #pragma unroll
-  for (int h = 0; h < kMaxGroup; ++h)
+  for (int h = 0; h < G; ++h) {
+    const float4 a = *reinterpret_cast<const float4*>(&qs[h][sub * 8]);
+    const float4 b = *reinterpret_cast<const float4*>(&qs[h][sub * 8 + 4]);
+    q[h][0] = a.x; q[h][1] = a.y; q[h][2] = a.z; q[h][3] = a.w;
+    q[h][4] = b.x; q[h][5] = b.y; q[h][6] = b.z; q[h][7] = b.w;
+  }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qr[h][e] = h < G ? qs[h][sub * 8 + e] : 0.f;
-
-  // scores
-  for (int j0 = start; j0 < end; j0 += PPB) {
-    const int j = j0 + wave * PPW + pg;
-    float kk[8];
-    if (j < end) {
-      if (j == pos) {
+  for (int i = 0; i < NP; ++i) {
+    const int j = start + i * PPB + wave * PPW + pg;
+    if (j == pos) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) kk[e] = knew[sub * 8 + e];
-      } else {
-        load8(base + kv_off(kv, j, 0, g) + sub * 8, kk);
-      }
-    } else {
+      for (int e = 0; e < 8; ++e) { kr[i][e] = knew[sub * 8 + e]; vr[i][e] = vnew[sub * 8 + e]; }
+    } else if (j >= end) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) kk[e] = 0.f;
+      for (int e = 0; e < 8; ++e) { kr[i][e] = 0.f; vr[i][e] = 0.f; }
+    }
+    float s[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      s[h] = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[h] += q[h][e] * kr[i][e];
     }
 #pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h) {
-      if (h < G) {
-        float s = 0.f;
+    for (int h = 0; h < G; ++h) s[h] = group_sum<LPP>(s[h]);
+    if (sub == 0 && j < end) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s += qr[h][e] * kk[e];
-#pragma unroll
-        for (int m = LPP / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m);
-        if (sub == 0 && j < end) sc[h][j - start] = s;
-      }
+      for (int h = 0; h < G; ++h) sc[h][j - start] = s[h];
     }
   }
   __syncthreads();
 
-  // softmax statistics per head (one wave per head)
+  // ---- softmax statistics (one wave per head) ----------------------------------------
   const int len = end - start;
-  for (int h = wave; h < G; h += 4) {
-    float m = -INFINITY;
-    for (int i = lane; i < len; i += 64) m = fmaxf(m, sc[h][i]);
-    m = wave_max(m);
-    float l = 0.f;
-    for (int i = lane; i < len; i += 64) {
-      const float p = expf(sc[h][i] - m);
-      sc[h][i] = p;
-      l += p;
+#pragma unroll
+  for (int h0 = 0; h0 < G; h0 += 4) {
+    const int h = h0 + wave;
+    if (h < G) {
+      const float v = lane < len ? sc[h][lane] : -INFINITY;
+      const float m = wave_max(v);
+      const float p = lane < len ? __expf(v - m) : 0.f;
+      if (lane < len) sc[h][lane] = p;
+      const float l = wave_sum(p);
+      if (lane == 0) { mls[h][0] = m; mls[h][1] = l; }
     }
-    l = wave_sum(l);
-    if (lane == 0) { mls[h][0] = m; mls[h][1] = l; }
   }
   __syncthreads();
 
-  // weighted values
-  float acc[kMaxGroup][8];
+  // ---- weighted values -----------------------------------------------------------------
+  float acc[G][8];
 #pragma unroll
-  for (int h = 0; h < kMaxGroup; ++h)
+  for (int h = 0; h < G; ++h)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-  for (int j0 = start; j0 < end; j0 += PPB) {
-    const int j = j0 + wave * PPW + pg;
-    if (j < end) {
-      float vv[8];
-      if (j == pos) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) vv[e] = vnew[sub * 8 + e];
-      } else {
-        load8(base + kv_off(kv, j, 1, g) + sub * 8, vv);
-      }
+  for (int i = 0; i < NP; ++i) {
+    const int j = start + i * PPB + wave * PPW + pg;
+    const int jj = j < end ? j - start : 0;
+    const bool ok = j < end;
 #pragma unroll
-      for (int h = 0; h < kMaxGroup; ++h) {
-        if (h < G) {
-          const float p = sc[h][j - start];
+    for (int h = 0; h < G; ++h) {
+      const float p = ok ? sc[h][jj] : 0.f;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[h][e] += p * vv[e];
-        }
-      }
+      for (int e = 0; e < 8; ++e) acc[h][e] += p * vr[i][e];
     }
   }
+  // sum the positions held by the wave's rows (lanes 16 or 32 apart share a slice)
 #pragma unroll
-  for (int h = 0; h < kMaxGroup; ++h) {
-    if (h < G) {
+  for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float a = acc[h][e];
+    for (int e = 0; e < 8; ++e) {
+      float a = acc[h][e];
 #pragma unroll
-        for (int m = LPP; m < 64; m <<= 1) a += __shfl_xor(a, m);
-        if (pg == 0) accs[wave][h][sub * 8 + e] = a;
-      }
+      for (int m = LPP; m < 64; m <<= 1) a += __shfl_xor(a, m);
+      acc[h][e] = a;
+    }
+  if (pg == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      *reinterpret_cast<float4*>(&accs[wave][h][sub * 8]) =
+          make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
+      *reinterpret_cast<float4*>(&accs[wave][h][sub * 8 + 4]) =
+          make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
     }
   }
   __syncthreads();
@@ -200,46 +219,93 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
   }
 }
 
-// out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s
+// out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s over the active
+// splits s of head h (grid Hq, HD threads).
 template <int HD>
-__global__ __launch_bounds__(HD) void k_attn_combine(const float* __restrict__ part_o,
-                                                     const float* __restrict__ part_ml,
-                                                     int nsplit, float* __restrict__ out) {
-  const int h = blockIdx.x, d = threadIdx.x;
+__global__ __launch_bounds__(HD) void k_attn_merge(const float* __restrict__ part_o,
+                                                   const float* __restrict__ part_ml,
+                                                   int nsplit, const DecodeState* __restrict__ st,
+                                                   float* __restrict__ out) {
+  __shared__ float w[kMaxSplits];
+  __shared__ float red[HD / 64];
+  const int h = blockIdx.x, d = threadIdx.x, lane = d & 63, wv = d >> 6;
+  const int active = (st->pos + kChunk) / kChunk;  // ceil((pos + 1) / chunk)
   const float* ml = part_ml + (size_t)h * nsplit * 2;
-  float M = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, ml[2 * s]);
-  float L = 0.f, o = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const float w = expf(ml[2 * s] - M);
-    L += w * ml[2 * s + 1];
-    o += w * part_o[((size_t)h * nsplit + s) * HD + d];
+  float mloc = -INFINITY;
+  for (int s = d; s < active; s += HD) mloc = fmaxf(mloc, ml[2 * s]);
+  mloc = wave_max(mloc);
+  if (lane == 0) red[wv] = mloc;
+  __syncthreads();
+  float M = red[0];
+#pragma unroll
+  for (int i = 1; i < HD / 64; ++i) M = fmaxf(M, red[i]);
+  float lsum = 0.f;
+  for (int s = d; s < active; s += HD) {
+    const float e = __expf(ml[2 * s] - M);
+    w[s] = e;
+    lsum += e * ml[2 * s + 1];
   }
+  lsum = wave_sum(lsum);
+  __syncthreads();
+  if (lane == 0) red[wv] = lsum;
+  __syncthreads();
+  float L = 0.f;
+#pragma unroll
+  for (int i = 0; i < HD / 64; ++i) L += red[i];
+  const float* po = part_o + (size_t)h * nsplit * HD + d;
+  float o = 0.f;
+  int s = 0;
+  for (; s + 4 <= active; s += 4) {
+    const float a0 = po[(size_t)(s + 0) * HD], a1 = po[(size_t)(s + 1) * HD];
+    const float a2 = po[(size_t)(s + 2) * HD], a3 = po[(size_t)(s + 3) * HD];
+    o += w[s] * a0 + w[s + 1] * a1 + w[s + 2] * a2 + w[s + 3] * a3;
+  }
+  for (; s < active; ++s) o += w[s] * po[(size_t)s * HD];
   out[(size_t)h * HD + d] = o / L;
 }
 
-template <int HD, typename KT>
+template <int HD, typename KT, int G>
 static hipError_t attn_decode_t(const float* qkv, int Hq, const float* cos_t, const float* sin_t,
                                 KvLayout kv, const DecodeState* st, int nsplit, float* part_o,
                                 float* part_ml, float* out, hipStream_t s) {
-  hipLaunchKernelGGL((k_attn_decode<HD, KT>), dim3(nsplit, kv.n_kv), dim3(256), 0, s, qkv, Hq,
-                     cos_t, sin_t, kv, st, nsplit, part_o, part_ml);
-  hipLaunchKernelGGL((k_attn_combine<HD>), dim3(Hq), dim3(HD), 0, s, part_o, part_ml, nsplit,
+  hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv), dim3(256), 0, s, qkv,
+                     Hq, cos_t, sin_t, kv, st, part_o, part_ml);
+  hipLaunchKernelGGL((k_attn_merge<HD>), dim3(Hq), dim3(HD), 0, s, part_o, part_ml, nsplit, st,
                      out);
   return hipGetLastError();
 }
 
+template <int HD, typename KT>
+static hipError_t attn_decode_g(int G, const float* qkv, int Hq, const float* cos_t,
+                                const float* sin_t, KvLayout kv, const DecodeState* st,
+                                int nsplit, float* part_o, float* part_ml, float* out,
+                                hipStream_t s) {
+  switch (G) {
+    case 1: return attn_decode_t<HD, KT, 1>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    case 2: return attn_decode_t<HD, KT, 2>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    case 4: return attn_decode_t<HD, KT, 4>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    case 5: return attn_decode_t<HD, KT, 5>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    case 8: return attn_decode_t<HD, KT, 8>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+int attn_decode_splits(int max_seq) { return (max_seq + kChunk - 1) / kChunk; }
+bool attn_group_supported(int G) { return G == 1 || G == 2 || G == 4 || G == 5 || G == 8; }
+
 hipError_t launch_attn_decode(bool kv_bf16, const float* qkv, int Hq, const float* cos_t,
                               const float* sin_t, KvLayout kv, const void* state, int nsplit,
                               float* part_o, float* part_ml, float* out, hipStream_t s) {
+  if (nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos) return hipErrorInvalidValue;
   const DecodeState* st = static_cast<const DecodeState*>(state);
+  const int G = Hq / kv.n_kv;
   if (kv.hd == 128) {
-    if (kv_bf16) return attn_decode_t<128, bf16_t>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
-    return attn_decode_t<128, float>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    if (kv_bf16) return attn_decode_g<128, bf16_t>(G, qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    return attn_decode_g<128, float>(G, qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
   }
   if (kv.hd == 64) {
-    if (kv_bf16) return attn_decode_t<64, bf16_t>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
-    return attn_decode_t<64, float>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    if (kv_bf16) return attn_decode_g<64, bf16_t>(G, qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    return attn_decode_g<64, float>(G, qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
   }
   return hipErrorInvalidValue;
 }

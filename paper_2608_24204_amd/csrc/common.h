@@ -52,16 +52,43 @@ __device__ __forceinline__ void load8(const float* p, float* o) {
   o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+// ---- cross-lane reductions -------------------------------------------------------
+// DPP row operations move data between lanes of a 16-lane row inside the VALU
+// (a few cycles) instead of through the LDS crossbar (ds_bpermute, ~100 cycles).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xb1;         // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4e;         // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // lane i <-> 7-i within each 8 lanes
+constexpr int kDppMirror = 0x140;      // lane i <-> 15-i within each 16 lanes
+
+// Sum over aligned groups of N lanes (N = 2, 4, 8, 16, 32 or 64); every lane of a
+// group receives the group's sum.
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  if (N >= 2) v += dpp<kDppXor1>(v);
+  if (N >= 4) v += dpp<kDppXor2>(v);
+  if (N >= 8) v += dpp<kDppHalfMirror>(v);
+  if (N >= 16) v += dpp<kDppMirror>(v);
+  if (N >= 32) v += __shfl_xor(v, 16);
+  if (N >= 64) v += __shfl_xor(v, 32);
   return v;
 }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
+template <int N>
+__device__ __forceinline__ float group_max(float v) {
+  if (N >= 2) v = fmaxf(v, dpp<kDppXor1>(v));
+  if (N >= 4) v = fmaxf(v, dpp<kDppXor2>(v));
+  if (N >= 8) v = fmaxf(v, dpp<kDppHalfMirror>(v));
+  if (N >= 16) v = fmaxf(v, dpp<kDppMirror>(v));
+  if (N >= 32) v = fmaxf(v, __shfl_xor(v, 16));
+  if (N >= 64) v = fmaxf(v, __shfl_xor(v, 32));
   return v;
 }
+
+__device__ __forceinline__ float wave_sum(float v) { return group_sum<64>(v); }
+__device__ __forceinline__ float wave_max(float v) { return group_max<64>(v); }
 
 // Sum over a 256-thread block; every thread gets the result.  `red` holds >= 4 floats.
 __device__ __forceinline__ float block256_sum(float v, float* red) {

@@ -1,107 +1,193 @@
 // Weight-streaming GEMV for the batch-1 decode step (y = W x).
 //
 // Decode is bound by HBM bandwidth: every weight byte is read once per token
-// and used for one multiply-add.  The kernel therefore only has to keep enough
-// 16-byte loads in flight on every CU and waste none of the bytes:
-//  - a persistent grid of 256-thread workgroups; each workgroup first stages the
-//    fp32 input vector in LDS (optionally RMS-normalised and scaled by the norm
-//    gain, the sum of squares being recomputed per workgroup so no extra launch
-//    or grid-wide reduction is needed);
-//  - each wavefront owns complete rows, two at a time (a gate/up pair for the
-//    SwiGLU epilogue), and streams them with 64 lanes x 16 B = 1 KiB fully
-//    coalesced loads, unrolled so that up to 16 loads per lane are in flight;
-//  - a row's 64 partial sums are reduced with cross-lane shuffles; there are no
-//    barriers after the staging step, so wavefronts never wait for each other.
+// and used for one multiply-add.  On MI355X the DRAM side streams fastest when
+// the whole chip reads one sliding, contiguous window of memory with a modest
+// number of non-temporal 16-byte loads in flight per lane (measured: ~7.2 TB/s
+// with one 256-thread workgroup per CU and eight loads per lane, against
+// 5.4-6.5 TB/s for more workgroups or scattered row streams).  The kernel is
+// shaped after that:
+//  - a persistent grid (one or two workgroups per CU); wavefront w of the grid
+//    owns row groups w, w + W, w + 2W, ... (W wavefronts in all), so at any time
+//    the chip streams a contiguous band of rows;
+//  - a row group is ROWS complete rows (two for a gate/up pair of the SwiGLU
+//    epilogue) read with 64 lanes x 16 B = 1 KiB coalesced loads, in batches of
+//    U sweeps of 512 elements; the next batch is issued before the current one
+//    is consumed (double buffering), so loads never stop at row boundaries;
+//  - the first batch is issued before the prologue, which stages x * gain in
+//    LDS; an RMS-normalised input gets its 1/rms factor applied to the finished
+//    row sums (W (x g r) = r W (x g)), so one barrier publishes the vector;
+//  - row sums are reduced with DPP row operations; after the prologue no
+//    wavefront ever waits for another.
 #include "common.h"
 #include "kernels.h"
 
 namespace wici {
 
-template <typename WT, int EPI, bool NORM>
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+template <typename WT> struct Vec8;   // 8 weights
+template <> struct Vec8<bf16_t> { u32x4 a; };
+template <> struct Vec8<float> { u32x4 a, b; };
+
+// Weights are read exactly once per step: non-temporal loads keep them from
+// displacing the small vectors that are reused from the caches.
+__device__ __forceinline__ void ld(Vec8<bf16_t>& v, const bf16_t* p) {
+  v.a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ void ld(Vec8<float>& v, const float* p) {
+  v.a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  v.b = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p) + 1);
+}
+__device__ __forceinline__ void zero(Vec8<bf16_t>& v) { v.a = u32x4{0, 0, 0, 0}; }
+__device__ __forceinline__ void zero(Vec8<float>& v) { v.a = u32x4{0, 0, 0, 0}; v.b = v.a; }
+__device__ __forceinline__ float dot8(const Vec8<bf16_t>& v, const float* x) {
+  const float4 xa = *reinterpret_cast<const float4*>(x);
+  const float4 xb = *reinterpret_cast<const float4*>(x + 4);
+  return __uint_as_float(v.a.x << 16) * xa.x + __uint_as_float(v.a.x & 0xffff0000u) * xa.y +
+         __uint_as_float(v.a.y << 16) * xa.z + __uint_as_float(v.a.y & 0xffff0000u) * xa.w +
+         __uint_as_float(v.a.z << 16) * xb.x + __uint_as_float(v.a.z & 0xffff0000u) * xb.y +
+         __uint_as_float(v.a.w << 16) * xb.z + __uint_as_float(v.a.w & 0xffff0000u) * xb.w;
+}
+__device__ __forceinline__ float dot8(const Vec8<float>& v, const float* x) {
+  const float4 xa = *reinterpret_cast<const float4*>(x);
+  const float4 xb = *reinterpret_cast<const float4*>(x + 4);
+  return __uint_as_float(v.a.x) * xa.x + __uint_as_float(v.a.y) * xa.y +
+         __uint_as_float(v.a.z) * xa.z + __uint_as_float(v.a.w) * xa.w +
+         __uint_as_float(v.b.x) * xb.x + __uint_as_float(v.b.y) * xb.y +
+         __uint_as_float(v.b.z) * xb.z + __uint_as_float(v.b.w) * xb.w;
+}
+
+// Batch b of a wavefront = (row group, first sweep); nsb batches per group.
+template <typename WT, int ROWS, int U>
+struct Batch {
+  Vec8<WT> w[ROWS][U];
+};
+
+template <typename WT, int EPI, bool NORM, int ROWS, int U>
 __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, int K,
                                               const float* __restrict__ x,
                                               const float* __restrict__ gain, float eps,
                                               float* __restrict__ y,
                                               ArgmaxPart* __restrict__ part) {
+  static_assert(EPI != GEMV_SWIGLU || ROWS % 2 == 0, "SwiGLU needs whole gate/up pairs");
   extern __shared__ float xs[];  // K floats
   __shared__ float red[4];
   __shared__ float am_v[4];
   __shared__ int am_i[4];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int nsweep = (K + 511) >> 9;          // 512-element sweeps per row
+  const int nsb = (nsweep + U - 1) / U;       // batches per row group
+  const int ngroups = (N + ROWS - 1) / ROWS;
+  const int wid = blockIdx.x * 4 + wave, nw = gridDim.x * 4;
+  const int my_groups = wid < ngroups ? (ngroups - 1 - wid) / nw + 1 : 0;
+  const int nbatch = my_groups * nsb;
 
-  // ---- stage x (optionally normalised) in LDS --------------------------------
+  // issue batch b into buf (rows past N and lanes past K read nothing)
+  auto issue = [&](Batch<WT, ROWS, U>& buf, int b) {
+    const int gi = b / nsb, s0 = (b - gi * nsb) * U;
+    const int r0 = (wid + gi * nw) * ROWS;
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+      const WT* wr = W + (size_t)min(r0 + r, N - 1) * K + lane * 8;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = (s0 + u) * 512 + lane * 8;
+        if (r0 + r < N && k < K) ld(buf.w[r][u], wr + (s0 + u) * 512);
+        else zero(buf.w[r][u]);
+      }
+    }
+  };
+
+  Batch<WT, ROWS, U> b0, b1;
+  if (nbatch > 0) issue(b0, 0);
+
+  // ---- stage x * gain in LDS, sum of squares for the norm ---------------------------
   float ss = 0.f;
-  for (int k = tid * 4; k < K; k += 1024) {
-    float4 v = *reinterpret_cast<const float4*>(x + k);
-    *reinterpret_cast<float4*>(xs + k) = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-  }
-  if (NORM) {
-    const float tot = block256_sum(ss, red);
-    const float r = 1.0f / sqrtf(tot / (float)K + eps);
-    for (int k = tid * 4; k < K; k += 1024) {
-      float4 v = *reinterpret_cast<float4*>(xs + k);
-      float4 g = *reinterpret_cast<const float4*>(gain + k);
-      v.x = v.x * r * g.x; v.y = v.y * r * g.y; v.z = v.z * r * g.z; v.w = v.w * r * g.w;
-      *reinterpret_cast<float4*>(xs + k) = v;
+  {
+    constexpr int SU = 4;
+    for (int k0 = tid * 4; k0 < K; k0 += 1024 * SU) {
+      float4 v[SU];
+#pragma unroll
+      for (int u = 0; u < SU; ++u)
+        if (k0 + u * 1024 < K) v[u] = *reinterpret_cast<const float4*>(x + k0 + u * 1024);
+#pragma unroll
+      for (int u = 0; u < SU; ++u) {
+        const int k = k0 + u * 1024;
+        if (k < K) {
+          float4 t = v[u];
+          if (NORM) {
+            ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
+            const float4 g = *reinterpret_cast<const float4*>(gain + k);
+            t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
+          }
+          *reinterpret_cast<float4*>(xs + k) = t;
+        }
+      }
     }
   }
+  if (NORM) {
+    ss = wave_sum(ss);
+    if (lane == 0) red[wave] = ss;
+  }
   __syncthreads();
+  const float rnorm = NORM ? 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)K + eps)
+                           : 1.0f;
 
-  // ---- stream row pairs --------------------------------------------------------
-  const int npairs = (N + 1) >> 1;
-  const int nwaves = gridDim.x * 4;
-  const int nfull = K >> 9;               // full 512-element sweeps of the wave
-  const bool tail = (nfull << 9) + lane * 8 < K;
+  float acc[ROWS];
+#pragma unroll
+  for (int r = 0; r < ROWS; ++r) acc[r] = 0.f;
   float best_v = -INFINITY;
   int best_i = 0x7fffffff;
   bool bad = false;
 
-  for (int p = blockIdx.x * 4 + wave; p < npairs; p += nwaves) {
-    const int r0 = 2 * p;
-    const bool has1 = r0 + 1 < N;
-    const WT* w0 = W + (size_t)r0 * K + lane * 8;
-    const WT* w1 = has1 ? w0 + K : w0;
-    const float* xl = xs + lane * 8;
-    float a0 = 0.f, a1 = 0.f;
-#pragma unroll 8
-    for (int it = 0; it < nfull; ++it) {
-      float u[8], v[8];
-      load8(w0 + it * 512, u);
-      load8(w1 + it * 512, v);
-      const float4 xa = *reinterpret_cast<const float4*>(xl + it * 512);
-      const float4 xb = *reinterpret_cast<const float4*>(xl + it * 512 + 4);
-      a0 += u[0] * xa.x + u[1] * xa.y + u[2] * xa.z + u[3] * xa.w +
-            u[4] * xb.x + u[5] * xb.y + u[6] * xb.z + u[7] * xb.w;
-      a1 += v[0] * xa.x + v[1] * xa.y + v[2] * xa.z + v[3] * xa.w +
-            v[4] * xb.x + v[5] * xb.y + v[6] * xb.z + v[7] * xb.w;
-    }
-    if (tail) {
-      float u[8], v[8];
-      load8(w0 + nfull * 512, u);
-      load8(w1 + nfull * 512, v);
-      const float* xt = xl + nfull * 512;
+  auto consume = [&](const Batch<WT, ROWS, U>& buf, int b) {
+    const int gi = b / nsb, sb = b - gi * nsb, s0 = sb * U;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) { a0 += u[e] * xt[e]; a1 += v[e] * xt[e]; }
-    }
-    a0 = wave_sum(a0);
-    a1 = wave_sum(a1);
-    if (EPI == GEMV_SWIGLU) {
-      if (lane == 0) y[p] = silu(a0) * a1;
-    } else if (EPI == GEMV_RESID) {
-      if (lane == 0) y[r0] += a0;
-      if (lane == 1 && has1) y[r0 + 1] += a1;
-    } else {
-      if (lane == 0) y[r0] = a0;
-      if (lane == 1 && has1) y[r0 + 1] = a1;
-      if (EPI == GEMV_ARGMAX) {
-        // NaN never compares better; the final pass detects non-finite logits
-        if (am_better(a0, r0, best_v, best_i)) { best_v = a0; best_i = r0; }
-        if (has1 && am_better(a1, r0 + 1, best_v, best_i)) { best_v = a1; best_i = r0 + 1; }
-        bad |= !isfinite(a0) || (has1 && !isfinite(a1));
+    for (int u = 0; u < U; ++u) {
+      const int k = (s0 + u) * 512 + lane * 8;
+      if (k < K) {
+        const float* xk = xs + k;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) acc[r] += dot8(buf.w[r][u], xk);
       }
     }
+    if (sb == nsb - 1) {  // row group complete
+      const int r0 = (wid + gi * nw) * ROWS;
+#pragma unroll
+      for (int r = 0; r < ROWS; ++r) acc[r] = wave_sum(acc[r]) * rnorm;
+      if (EPI == GEMV_SWIGLU) {
+#pragma unroll
+        for (int r = 0; r < ROWS; r += 2)
+          if (lane == r && r0 + r + 1 < N) y[(r0 + r) >> 1] = silu(acc[r]) * acc[r + 1];
+      } else {
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+          if (lane == r && r0 + r < N) {
+            if (EPI == GEMV_RESID) y[r0 + r] += acc[r];
+            else y[r0 + r] = acc[r];
+          }
+          if (EPI == GEMV_ARGMAX && r0 + r < N) {
+            // NaN never compares better; a non-finite logit is flagged separately
+            if (am_better(acc[r], r0 + r, best_v, best_i)) { best_v = acc[r]; best_i = r0 + r; }
+            bad |= !isfinite(acc[r]);
+          }
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < ROWS; ++r) acc[r] = 0.f;
+    }
+  };
+
+  // double-buffered stream of batches: issue b+1, consume b
+  for (int b = 0; b < nbatch; b += 2) {
+    if (b + 1 < nbatch) issue(b1, b + 1);
+    consume(b0, b);
+    if (b + 1 < nbatch) {
+      if (b + 2 < nbatch) issue(b0, b + 2);
+      consume(b1, b + 1);
+    }
   }
+
   if (EPI == GEMV_ARGMAX) {
     // a non-finite logit marks the partial with index -1
     if (lane == 0) { am_v[wave] = best_v; am_i[wave] = bad ? -1 : best_i; }
@@ -119,46 +205,67 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
   }
 }
 
-static int gemv_grid(int N) {
-  const int npairs = (N + 1) / 2;
-  int g = (npairs + 3) / 4;  // one pair per wavefront
-  if (g > 1024) g = 1024;
-  if (g < 1) g = 1;
-  return g;
+// Launch shape: ROWS rows per group, U sweeps per batch, `grid` workgroups.
+template <typename WT, int EPI, int ROWS, int U>
+hipError_t launch_gemv_cfg(const WT* W, int N, int K, const float* x, const float* gain,
+                           float eps, float* y, ArgmaxPart* part, int grid, hipStream_t st) {
+  const size_t lds = (size_t)K * sizeof(float);
+#define WICI_GEMV_NORM(NR)                                                                   \
+  do {                                                                                       \
+    if (lds > 65536)                                                                         \
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemv<WT, EPI, NR, ROWS, U>), \
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);       \
+    hipLaunchKernelGGL((k_gemv<WT, EPI, NR, ROWS, U>), dim3(grid), dim3(256), lds, st, W, N, K, \
+                       x, gain, eps, y, part);                                               \
+  } while (0)
+  if (gain) WICI_GEMV_NORM(true);
+  else WICI_GEMV_NORM(false);
+#undef WICI_GEMV_NORM
+  return hipGetLastError();
 }
 
-int gemv_argmax_blocks(int N) { return gemv_grid(N); }
+// Launch shape per matrix: two rows per group, 4 sweeps (2 KiB of bf16 per row)
+// per batch, two workgroups per CU; one workgroup per CU when the staged vector
+// is too large for two.  (From a sweep of group rows {1,2,4}, sweeps per batch
+// {2,4,8} and 256..1024 workgroups over the decode matrices of the 8B shape.)
+struct GemvShape { int grid; };
+
+static GemvShape gemv_shape(int N, int K) {
+  GemvShape s{(size_t)K * 4 > 80 * 1024 ? 256 : 512};
+  const int need = ((N + 1) / 2 + 3) / 4;  // workgroups for one group per wavefront
+  if (need < s.grid) s.grid = need < 1 ? 1 : need;
+  return s;
+}
+
+int gemv_argmax_blocks(int N) { return gemv_shape(N, 0).grid; }
+
+template <typename WT, int EPI>
+static hipError_t gemv_dispatch(const GemvShape& s, const WT* W, int N, int K, const float* x,
+                                const float* gain, float eps, float* y, ArgmaxPart* part,
+                                hipStream_t st) {
+  // the same bytes per batch for both weight types
+  if (sizeof(WT) == 2)
+    return launch_gemv_cfg<WT, EPI, 2, 4>(W, N, K, x, gain, eps, y, part, s.grid, st);
+  return launch_gemv_cfg<WT, EPI, 2, 2>(W, N, K, x, gain, eps, y, part, s.grid, st);
+}
 
 template <typename WT>
-static hipError_t gemv_t(int epi, const WT* W, int N, int K, const float* x,
-                         const float* gain, float eps, float* y, ArgmaxPart* part,
-                         hipStream_t st) {
-  const int g = gemv_grid(N);
-  const size_t lds = (size_t)K * sizeof(float);
-  const bool nrm = gain != nullptr;
-#define WICI_GEMV(E, NR)                                                                  \
-  do {                                                                                    \
-    if (lds > 65536)                                                                      \
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemv<WT, E, NR>),        \
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);    \
-    hipLaunchKernelGGL((k_gemv<WT, E, NR>), dim3(g), dim3(256), lds, st, W, N, K, x, gain, \
-                       eps, y, part);                                                     \
-  } while (0)
+static hipError_t gemv_t(int epi, const WT* W, int N, int K, const float* x, const float* gain,
+                         float eps, float* y, ArgmaxPart* part, hipStream_t st) {
+  const GemvShape s = gemv_shape(N, K);
   switch (epi) {
-    case GEMV_STORE: if (nrm) WICI_GEMV(GEMV_STORE, true); else WICI_GEMV(GEMV_STORE, false); break;
-    case GEMV_RESID: if (nrm) WICI_GEMV(GEMV_RESID, true); else WICI_GEMV(GEMV_RESID, false); break;
-    case GEMV_SWIGLU: if (nrm) WICI_GEMV(GEMV_SWIGLU, true); else WICI_GEMV(GEMV_SWIGLU, false); break;
-    case GEMV_ARGMAX: if (nrm) WICI_GEMV(GEMV_ARGMAX, true); else WICI_GEMV(GEMV_ARGMAX, false); break;
+    case GEMV_STORE: return gemv_dispatch<WT, GEMV_STORE>(s, W, N, K, x, gain, eps, y, part, st);
+    case GEMV_RESID: return gemv_dispatch<WT, GEMV_RESID>(s, W, N, K, x, gain, eps, y, part, st);
+    case GEMV_SWIGLU: return gemv_dispatch<WT, GEMV_SWIGLU>(s, W, N, K, x, gain, eps, y, part, st);
+    case GEMV_ARGMAX: return gemv_dispatch<WT, GEMV_ARGMAX>(s, W, N, K, x, gain, eps, y, part, st);
     default: return hipErrorInvalidValue;
   }
-#undef WICI_GEMV
-  return hipGetLastError();
 }
 
 hipError_t launch_gemv(bool w_bf16, int epi, const void* W, int N, int K, const float* x,
                        const float* norm_gain, float eps, float* y, ArgmaxPart* part,
                        int* nblocks, hipStream_t st) {
-  if (nblocks) *nblocks = gemv_grid(N);
+  if (nblocks) *nblocks = gemv_shape(N, K).grid;
   if (w_bf16)
     return gemv_t<bf16_t>(epi, static_cast<const bf16_t*>(W), N, K, x, norm_gain, eps, y, part, st);
   return gemv_t<float>(epi, static_cast<const float*>(W), N, K, x, norm_gain, eps, y, part, st);

@@ -43,6 +43,7 @@ struct KvLayout {
   int page;              // positions per page
   int n_kv;              // KV heads
   int hd;                // head dim
+  int max_pos;           // capacity (positions); the table covers ceil(max_pos / page) pages
   // element offset of (phys page, kv 0/1, head h, slot s, dim d):
   //   ((phys * 2 + kv) * n_kv + h) * page * hd + s * hd + d
 };
@@ -59,12 +60,14 @@ hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, in
                                KvLayout kv, float* out, hipStream_t st);
 
 // Decode attention at position state->pos: rotates q and the new k, appends the
-// new k, v, attends over [0, pos] in nsplit splits, then combines into out
-// [Hq*hd] fp32.
+// new k, v, attends over [0, pos] in splits of 64 positions (grid nsplit x Hkv,
+// nsplit = attn_decode_splits(max_seq)) and merges them into out [Hq*hd] fp32.
 hipError_t launch_attn_decode(bool kv_bf16, const float* qkv, int Hq, const float* cos_t,
                               const float* sin_t, KvLayout kv, const void* state,
                               int nsplit, float* part_o, float* part_ml, float* out,
                               hipStream_t st);
+int attn_decode_splits(int max_seq);
+bool attn_group_supported(int G);
 
 // C[M, N] (ldc) = A[M, K] (fp32, lda) x W[N, K]^T with epilogue as launch_gemv
 // (STORE / RESID / SWIGLU; SWIGLU writes C[M, N/2]).

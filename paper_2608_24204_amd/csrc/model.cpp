@@ -48,7 +48,10 @@ bool config_ok(const wici_config* c, std::string* why) {
   if (c->head_dim != 64 && c->head_dim != 128) return bad("head_dim must be 64 or 128");
   if (c->n_kv_heads < 1 || c->n_heads < 1 || c->n_heads % c->n_kv_heads)
     return bad("n_heads must be a positive multiple of n_kv_heads");
-  if (c->n_heads / c->n_kv_heads > 8) return bad("at most 8 query heads per KV head");
+  if (!wici::attn_group_supported(c->n_heads / c->n_kv_heads))
+    return bad("query heads per KV head must be 1, 2, 4, 5 or 8");
+  if (c->max_seq > 16384) return bad("max_seq above 16384");
+  if (c->n_heads > 128) return bad("at most 128 query heads");
   if (c->vocab < 1) return bad("vocab must be >= 1");
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return bad("rms_eps must be > 0");
   if (!(c->rope_base > 1.0) || !std::isfinite(c->rope_base)) return bad("rope_base must be > 1");
@@ -98,7 +101,7 @@ Layout make_layout(const wici_config& c) {
                                dsize(c.kv_dtype));
   L.kv_bytes = L.kv_layer_stride * c.n_layers;
 
-  L.nsplit = std::max(32, (c.max_seq + 255) / 256);
+  L.nsplit = wici::attn_decode_splits(c.max_seq);
   const size_t C = c.prefill_chunk;
   o = 0;
   L.x = o; o = align_up(o + C * d * 4);
@@ -161,6 +164,7 @@ struct wici_model {
     k.page = cfg.kv_page;
     k.n_kv = cfg.n_kv_heads;
     k.hd = cfg.head_dim;
+    k.max_pos = cfg.max_seq;
     return k;
   }
 };
