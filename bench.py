@@ -168,7 +168,7 @@ def main(argv=None):
         "decode_hbm_frac": bytes_tok * decode_tok_s / HBM_PEAK,
         "prefill_flops": pf_flops,
         "prefill_mfma_frac": pf_flops / (ttft_ms / 1e3) / MFMA_BF16_PEAK,
-        "prefill_mode": args.prefill_mode or ("f32" if cfg.weight_dtype == "f32" else "bf16x2"),
+        "prefill_mode": args.prefill_mode or ("f32" if cfg.weight_dtype == "f32" else "bf16x3"),
     }
 
     if not args.no_profile:

@@ -54,10 +54,12 @@ typedef enum { WICI_F32 = 0, WICI_BF16 = 1 } wici_dtype;
 /* Arithmetic of the prefill projections (decode always multiplies bf16/fp32
  * weights by fp32 activations with fp32 accumulation). */
 typedef enum {
-  WICI_PREFILL_BF16X2 = 0, /* MFMA bf16; fp32 activations split into hi+lo bf16
-                              terms (two products per tile): ~fp32-accurate */
-  WICI_PREFILL_BF16 = 1,   /* MFMA bf16; activations rounded to bf16 once */
-  WICI_PREFILL_F32 = 2     /* vector fp32 (required for fp32 weights) */
+  WICI_PREFILL_BF16X2 = 0, /* matrix cores, bf16; each fp32 activation stored as two
+                              bf16 terms (two products per tile), ~2^-16 relative */
+  WICI_PREFILL_BF16 = 1,   /* matrix cores, bf16; activations rounded to bf16 once */
+  WICI_PREFILL_F32 = 2,    /* vector fp32 (required for fp32 weights) */
+  WICI_PREFILL_BF16X3 = 3  /* matrix cores, bf16; three bf16 terms per activation
+                              (three products per tile), fp32-accurate */
 } wici_prefill_mode;
 
 enum { WICI_FLAG_NO_GRAPH = 1 }; /* run decode steps eagerly instead of replaying a graph */

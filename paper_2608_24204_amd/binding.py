@@ -22,7 +22,7 @@ WICI_OK, WICI_E_ARG, WICI_E_STATE, WICI_E_CAPACITY, WICI_E_HIP, WICI_E_NUMERIC =
 STATUS_NAMES = {0: "WICI_OK", -1: "WICI_E_ARG", -2: "WICI_E_STATE", -3: "WICI_E_CAPACITY",
                 -4: "WICI_E_HIP", -5: "WICI_E_NUMERIC"}
 WICI_F32, WICI_BF16 = 0, 1
-PREFILL_MODES = {"bf16x2": 0, "bf16": 1, "f32": 2}
+PREFILL_MODES = {"bf16x2": 0, "bf16": 1, "f32": 2, "bf16x3": 3}
 WICI_FLAG_NO_GRAPH = 1
 
 # every entry point include/wici.h declares
@@ -98,7 +98,7 @@ def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool =
                 max_seq: int | None = None, prefill_chunk: int | None = None,
                 kv_page: int | None = None) -> WiciConfig:
     if prefill_mode is None:
-        prefill_mode = "f32" if cfg.weight_dtype == "f32" else "bf16x2"
+        prefill_mode = "f32" if cfg.weight_dtype == "f32" else "bf16x3"
     c = WiciConfig()
     c.n_layers, c.d_model, c.n_heads = cfg.n_layers, cfg.d_model, cfg.n_heads
     c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab = cfg.n_kv_heads, cfg.head_dim, cfg.ffn_dim, cfg.vocab

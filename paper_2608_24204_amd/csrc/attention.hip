@@ -313,8 +313,7 @@ hipError_t launch_attn_decode(bool kv_bf16, const float* qkv, int Hq, const floa
 // ------------------------------------------------------------------- prefill
 template <int HD, typename KT>
 __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ qkv, int T,
-                                                      int p0, int Hq, KvLayout kv,
-                                                      float* __restrict__ out) {
+                                                      int p0, int Hq, KvLayout kv, ActBuf out) {
   constexpr int BQ = 64, BKEY = 64, DPT = HD / 4;
   __shared__ float Ks[BKEY][HD + 4];
   __shared__ float Vs[BKEY][HD + 4];
@@ -380,23 +379,23 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
     m = mn;
   }
   if (valid) {
-    float* o = out + (size_t)t * Hq * HD + (size_t)h * HD + part * DPT;
+    const size_t o = (size_t)t * Hq * HD + (size_t)h * HD + part * DPT;
     const float inv = 1.0f / l;
 #pragma unroll
-    for (int e = 0; e < DPT; ++e) o[e] = acc[e] * inv;
+    for (int e = 0; e < DPT; ++e) store_act(out, o + e, acc[e] * inv);
   }
 }
 
 template <int HD, typename KT>
 static hipError_t attn_prefill_t(const float* qkv, int T, int p0, int Hq, KvLayout kv,
-                                 float* out, hipStream_t s) {
+                                 const ActBuf& out, hipStream_t s) {
   hipLaunchKernelGGL((k_attn_prefill<HD, KT>), dim3((T + 63) / 64, Hq), dim3(256), 0, s, qkv, T,
                      p0, Hq, kv, out);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
-                               KvLayout kv, float* out, hipStream_t s) {
+                               KvLayout kv, const ActBuf& out, hipStream_t s) {
   if (kv.hd == 128) {
     if (kv_bf16) return attn_prefill_t<128, bf16_t>(qkv, T, p0, Hq, kv, out, s);
     return attn_prefill_t<128, float>(qkv, T, p0, Hq, kv, out, s);

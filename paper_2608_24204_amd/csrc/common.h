@@ -102,6 +102,32 @@ __device__ __forceinline__ float block256_sum(float v, float* red) {
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
+// Activation operands of the prefill matrix products.  With nt = 0 the values are
+// stored as fp32; with nt = 1..3 each fp32 value v is stored as nt bf16 terms in
+// separate planes (plane_stride elements apart): t0 = bf16(v), t1 = bf16(v - t0),
+// t2 = bf16(v - t0 - t1).  Each subtraction is exact in fp32, so three terms
+// carry v to about 2^-24 relative and the sum of the terms' products with exact
+// bf16 weights is an fp32-accurate product.
+struct ActBuf {
+  float* f32;         // nt == 0
+  bf16_t* planes;     // nt >= 1: [nt][rows][ld]
+  size_t plane_stride;
+  int nt;
+};
+
+__device__ __forceinline__ void store_act(const ActBuf& a, size_t idx, float v) {
+  if (a.nt == 0) {
+    a.f32[idx] = v;
+    return;
+  }
+  float r = v;
+  for (int p = 0; p < a.nt; ++p) {
+    const bf16_t t = f32_to_bf16(r);
+    a.planes[p * a.plane_stride + idx] = t;
+    r -= bf16_to_f32(t);
+  }
+}
+
 // Greedy-argmax order: larger value wins, lower index wins among equal values.
 __device__ __forceinline__ bool am_better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);

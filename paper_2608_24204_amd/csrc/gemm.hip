@@ -1,84 +1,108 @@
 // Prefill projections: C[M, N] = A[M, K] x W[N, K]^T with fused epilogues.
 //
-// A holds fp32 activations (one row per prompt position), W the bf16 weights in
-// their [out, in] layout, so both operands are contiguous along K, which is the
-// layout the gfx950 bf16 matrix cores consume (8 consecutive K values per lane).
+// A holds activations (one row per prompt position), W the bf16 weights in their
+// [out, in] layout, so both operands are contiguous along K, which is the layout
+// the gfx950 matrix cores consume (8 consecutive K values per lane).
 //
-// MFMA kernel: 128x128 output tile per 256-thread block (2x2 wavefronts of
-// 64x64, each a 4x4 grid of v_mfma_f32_16x16x32_bf16 tiles), K steps of 32
-// staged through LDS with the next step's global loads issued before the
-// current step's matrix ops.  The fp32 activations are converted to bf16 while
-// being staged; in the split mode each value a is stored as hi = bf16(a) and
-// lo = bf16(a - hi) and both are multiplied with the (exact) bf16 weights, which
-// keeps the product accurate to about 2^-16 relative instead of 2^-8.
+// MFMA kernel.  A arrives as NT bf16 planes whose sum is the fp32 activation
+// (see ActBuf); the weights are exact bf16, so the kernel accumulates the NT
+// products A_p W^T with v_mfma_f32_16x16x32_bf16 and the result carries the
+// activation's precision, not bf16's.  Tiling:
+//  - a block of WM x WN wavefronts owns a (64 WM) x (64 WN) output tile, each
+//    wavefront a 64 x 64 sub-tile (4 x 4 matrix-core tiles, 64 accumulator
+//    registers);
+//  - both operands are staged through LDS in 32-deep K steps, double-buffered
+//    (rows padded to 80 B so the 16 rows a fragment read touches fall in distinct
+//    banks); the next step's global loads are in flight while the current
+//    step's matrix ops run, one barrier a step;
+//  - tiles are numbered A-tile-row-major and dealt to the 8 XCDs in contiguous
+//    ranges (workgroups are dispatched round-robin over XCDs), so the blocks
+//    resident on one XCD share an A row-tile through that XCD's L2.
 //
-// Vector kernel: plain fp32 64x64 tiles, for fp32 weights.
+// Vector kernel: plain fp32 64x64 tiles, for fp32 weights / fp32 activations.
 #include "common.h"
 #include "kernels.h"
 
 namespace wici {
 
+// ------------------------------------------------------------------ epilogue
 template <int EPI>
-__device__ __forceinline__ void epi_store(float* C, int ldc, int M, int N, int m, int n,
-                                          float v, float other) {
+__device__ __forceinline__ void epi_out(float* C, int ldc, const ActBuf& H, int ldh, int M,
+                                        int N, int m, int n, float v, float other) {
   if (m >= M || n >= N) return;
   if (EPI == GEMV_STORE) C[(size_t)m * ldc + n] = v;
   else if (EPI == GEMV_RESID) C[(size_t)m * ldc + n] += v;
   else if (EPI == GEMV_SWIGLU) {
-    if (!(n & 1)) C[(size_t)m * ldc + (n >> 1)] = silu(v) * other;
+    if (!(n & 1)) store_act(H, (size_t)m * ldh + (n >> 1), silu(v) * other);
   }
 }
 
 // --------------------------------------------------------------------- MFMA
-template <bool SPLIT, int EPI>
-__global__ __launch_bounds__(256) void k_gemm_mfma(const float* __restrict__ A, int lda,
-                                                   const bf16_t* __restrict__ W, int M, int N,
-                                                   int K, float* __restrict__ C, int ldc) {
-  constexpr int BM = 128, BN = 128, BK = 32, LDK = BK + 8;
-  __shared__ __attribute__((aligned(16))) bf16_t As[BM][LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t Al[SPLIT ? BM : 1][LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[BN][LDK];
+constexpr int kBK = 32;   // K per step (one v_mfma_f32_16x16x32_bf16 depth)
+constexpr int kLDK = 40;  // padded LDS row (bf16 elements)
+
+template <int NT, int WM, int WN, int EPI>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
+    const bf16_t* __restrict__ A, size_t a_plane, int lda, const bf16_t* __restrict__ W, int M,
+    int N, int K, float* __restrict__ C, int ldc, ActBuf H, int ldh) {
+  constexpr int BM = 64 * WM, BN = 64 * WN, NTH = 64 * WM * WN;
+  constexpr int A_CHUNKS = NT * BM * (kBK / 8);  // 16-byte chunks per step
+  constexpr int W_CHUNKS = BN * (kBK / 8);
+  constexpr int A_PER = (A_CHUNKS + NTH - 1) / NTH;
+  constexpr int W_PER = (W_CHUNKS + NTH - 1) / NTH;
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+  bf16_t* As = smem;                            // [2][NT][BM][kLDK]
+  bf16_t* Bs = smem + 2 * NT * BM * kLDK;       // [2][BN][kLDK]
+
+  // ---- tile of this block (A-row-major tile order, contiguous ranges per XCD) ----
+  const int n_mt = (M + BM - 1) / BM, n_nt = (N + BN - 1) / BN, T = n_mt * n_nt;
+  const int per_xcd = (T + 7) / 8;
+  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= T) return;
+  const int m0 = (t / n_nt) * BM, n0 = (t % n_nt) * BN;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
 
-  const int lrow = tid >> 1, lk = (tid & 1) * 16;
-  const bool a_ok = m0 + lrow < M, w_ok = n0 + lrow < N;
-  const float* Ap = A + (size_t)(a_ok ? m0 + lrow : 0) * lda + lk;
-  const bf16_t* Wp = W + (size_t)(w_ok ? n0 + lrow : 0) * K + lk;
-
-  float4 ra[4];
-  uint4 rw[2];
+  uint4 ra[A_PER], rw[W_PER];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      ra[i] = a_ok ? *reinterpret_cast<const float4*>(Ap + k0 + 4 * i) : make_float4(0, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      rw[i] = w_ok ? *reinterpret_cast<const uint4*>(Wp + k0 + 8 * i) : make_uint4(0, 0, 0, 0);
-  };
-  auto sstore = [&]() {
-    const float* f = reinterpret_cast<const float*>(ra);
-    uint32_t hi[8], lo[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const bf16_t h0 = f32_to_bf16(f[2 * i]), h1 = f32_to_bf16(f[2 * i + 1]);
-      hi[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-      if (SPLIT) {
-        const bf16_t l0 = f32_to_bf16(f[2 * i] - bf16_to_f32(h0));
-        const bf16_t l1 = f32_to_bf16(f[2 * i + 1] - bf16_to_f32(h1));
-        lo[i] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    for (int i = 0; i < A_PER; ++i) {
+      const int c = tid + i * NTH;
+      if (c < A_CHUNKS) {
+        const int p = c / (BM * 4), row = (c / 4) % BM, part = c % 4;
+        const int m = m0 + row;
+        ra[i] = m < M ? *reinterpret_cast<const uint4*>(A + p * a_plane + (size_t)m * lda + k0 + part * 8)
+                      : make_uint4(0, 0, 0, 0);
       }
     }
-    *reinterpret_cast<uint4*>(&As[lrow][lk]) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-    *reinterpret_cast<uint4*>(&As[lrow][lk + 8]) = make_uint4(hi[4], hi[5], hi[6], hi[7]);
-    if (SPLIT) {
-      *reinterpret_cast<uint4*>(&Al[lrow][lk]) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-      *reinterpret_cast<uint4*>(&Al[lrow][lk + 8]) = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+#pragma unroll
+    for (int i = 0; i < W_PER; ++i) {
+      const int c = tid + i * NTH;
+      if (c < W_CHUNKS) {
+        const int row = c / 4, part = c % 4, n = n0 + row;
+        rw[i] = n < N ? *reinterpret_cast<const uint4*>(W + (size_t)n * K + k0 + part * 8)
+                      : make_uint4(0, 0, 0, 0);
+      }
     }
-    *reinterpret_cast<uint4*>(&Bs[lrow][lk]) = rw[0];
-    *reinterpret_cast<uint4*>(&Bs[lrow][lk + 8]) = rw[1];
+  };
+  auto sstore = [&](int s) {
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i) {
+      const int c = tid + i * NTH;
+      if (c < A_CHUNKS) {
+        const int p = c / (BM * 4), row = (c / 4) % BM, part = c % 4;
+        *reinterpret_cast<uint4*>(As + (((size_t)s * NT + p) * BM + row) * kLDK + part * 8) = ra[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < W_PER; ++i) {
+      const int c = tid + i * NTH;
+      if (c < W_CHUNKS) {
+        const int row = c / 4, part = c % 4;
+        *reinterpret_cast<uint4*>(Bs + ((size_t)s * BN + row) * kLDK + part * 8) = rw[i];
+      }
+    }
   };
 
   floatx4_t acc[4][4];
@@ -88,29 +112,32 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const float* __restrict__ A, 
     for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
   const int fr = lane & 15, fk = (lane >> 4) * 8;
+  const int KT = K / kBK;
   gload(0);
-  for (int k0 = 0; k0 < K; k0 += BK) {
-    __syncthreads();
-    sstore();
-    __syncthreads();
-    if (k0 + BK < K) gload(k0 + BK);
-    bf16x8_t af[4], al[4], bfr[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      af[i] = *reinterpret_cast<const bf16x8_t*>(&As[wm * 64 + i * 16 + fr][fk]);
-      if (SPLIT) al[i] = *reinterpret_cast<const bf16x8_t*>(&Al[wm * 64 + i * 16 + fr][fk]);
-    }
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < KT; ++kt) {
+    const int s = kt & 1;
+    if (kt + 1 < KT) gload((kt + 1) * kBK);
+    bf16x8_t bfr[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      bfr[j] = *reinterpret_cast<const bf16x8_t*>(&Bs[wn * 64 + j * 16 + fr][fk]);
+      bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + ((size_t)s * BN + wn * 64 + j * 16 + fr) * kLDK + fk);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int p = 0; p < NT; ++p) {
+      bf16x8_t af[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-        if (SPLIT)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[i], bfr[j], acc[i][j], 0, 0, 0);
-      }
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t*>(
+            As + (((size_t)s * NT + p) * BM + wm * 64 + i * 16 + fr) * kLDK + fk);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < KT) sstore(s ^ 1);
+    __syncthreads();
   }
 
   // lane holds rows 4*(lane/16)+r and column lane%16 of each 16x16 tile
@@ -124,7 +151,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const float* __restrict__ A, 
         const int n = n0 + wn * 64 + j * 16 + (lane & 15);
         const float v = acc[i][j][r];
         const float o = EPI == GEMV_SWIGLU ? __shfl_xor(v, 1) : 0.f;
-        epi_store<EPI>(C, ldc, M, N, m, n, v, o);
+        epi_out<EPI>(C, ldc, H, ldh, M, N, m, n, v, o);
       }
 }
 
@@ -132,7 +159,8 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const float* __restrict__ A, 
 template <typename WT, int EPI>
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, int lda,
                                                   const WT* __restrict__ W, int M, int N, int K,
-                                                  float* __restrict__ C, int ldc) {
+                                                  float* __restrict__ C, int ldc, ActBuf H,
+                                                  int ldh) {
   constexpr int BM = 64, BN = 64, BK = 16;
   __shared__ float As[BK][BM + 4];
   __shared__ float Ws[BK][BN + 4];
@@ -173,59 +201,80 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, i
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
-      epi_store<EPI>(C, ldc, M, N, m, n, acc[i][j], (j & 1) ? 0.f : acc[i][j + 1 < 4 ? j + 1 : j]);
+      epi_out<EPI>(C, ldc, H, ldh, M, N, m, n, acc[i][j], (j & 1) ? 0.f : acc[i][j | 1]);
     }
 }
 
-template <bool SPLIT>
-static hipError_t gemm_mfma_t(int epi, const float* A, int lda, const bf16_t* W, int M, int N,
-                              int K, float* C, int ldc, hipStream_t st) {
-  dim3 grid((N + 127) / 128, (M + 127) / 128);
-  switch (epi) {
-    case GEMV_STORE:
-      hipLaunchKernelGGL((k_gemm_mfma<SPLIT, GEMV_STORE>), grid, dim3(256), 0, st, A, lda, W, M, N, K, C, ldc);
-      break;
-    case GEMV_RESID:
-      hipLaunchKernelGGL((k_gemm_mfma<SPLIT, GEMV_RESID>), grid, dim3(256), 0, st, A, lda, W, M, N, K, C, ldc);
-      break;
-    case GEMV_SWIGLU:
-      hipLaunchKernelGGL((k_gemm_mfma<SPLIT, GEMV_SWIGLU>), grid, dim3(256), 0, st, A, lda, W, M, N, K, C, ldc);
-      break;
-    default: return hipErrorInvalidValue;
-  }
+// ------------------------------------------------------------------- launchers
+template <int NT, int WM, int WN, int EPI>
+static hipError_t gemm_mfma_launch(const ActBuf& A, int lda, const bf16_t* W, int M, int N, int K,
+                                   float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
+  constexpr int BM = 64 * WM, BN = 64 * WN;
+  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  const int grid = (tiles + 7) / 8 * 8;
+  const size_t lds = (size_t)2 * (NT * BM + BN) * kLDK * sizeof(bf16_t);
+  auto fn = &k_gemm_mfma<NT, WM, WN, EPI>;
+  if (lds > 65536)
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipLaunchKernelGGL(fn, dim3(grid), dim3(64 * WM * WN), lds, st, A.planes, A.plane_stride, lda,
+                     W, M, N, K, C, ldc, H, ldh);
   return hipGetLastError();
 }
 
-template <typename WT>
-static hipError_t gemm_f32_t(int epi, const float* A, int lda, const WT* W, int M, int N, int K,
-                             float* C, int ldc, hipStream_t st) {
+// Block shape: 256 x 128 when that still gives every CU a tile (fewer re-reads of
+// the weights), else 128 x 128.
+template <int NT, int EPI>
+static hipError_t gemm_mfma_nt(const ActBuf& A, int lda, const bf16_t* W, int M, int N, int K,
+                               float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
+  const long big_tiles = (long)((M + 255) / 256) * ((N + 127) / 128);
+  if (big_tiles >= 256)
+    return gemm_mfma_launch<NT, 4, 2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+  return gemm_mfma_launch<NT, 2, 2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+}
+
+template <int EPI>
+static hipError_t gemm_mfma(const ActBuf& A, int lda, const bf16_t* W, int M, int N, int K,
+                            float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
+  switch (A.nt) {
+    case 1: return gemm_mfma_nt<1, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+    case 2: return gemm_mfma_nt<2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+    case 3: return gemm_mfma_nt<3, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename WT, int EPI>
+static hipError_t gemm_f32(const ActBuf& A, int lda, const WT* W, int M, int N, int K, float* C,
+                           int ldc, const ActBuf& H, int ldh, hipStream_t st) {
   dim3 grid((N + 63) / 64, (M + 63) / 64);
-  switch (epi) {
-    case GEMV_STORE:
-      hipLaunchKernelGGL((k_gemm_f32<WT, GEMV_STORE>), grid, dim3(256), 0, st, A, lda, W, M, N, K, C, ldc);
-      break;
-    case GEMV_RESID:
-      hipLaunchKernelGGL((k_gemm_f32<WT, GEMV_RESID>), grid, dim3(256), 0, st, A, lda, W, M, N, K, C, ldc);
-      break;
-    case GEMV_SWIGLU:
-      hipLaunchKernelGGL((k_gemm_f32<WT, GEMV_SWIGLU>), grid, dim3(256), 0, st, A, lda, W, M, N, K, C, ldc);
-      break;
-    default: return hipErrorInvalidValue;
-  }
+  hipLaunchKernelGGL((k_gemm_f32<WT, EPI>), grid, dim3(256), 0, st, A.f32, lda, W, M, N, K, C,
+                     ldc, H, ldh);
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(int mode, bool w_bf16, int epi, const float* A, int lda, const void* W,
-                       int M, int N, int K, float* C, int ldc, hipStream_t st) {
-  if (mode == 0 || mode == 1) {
-    if (!w_bf16) return hipErrorInvalidValue;
-    const bf16_t* Wb = static_cast<const bf16_t*>(W);
-    return mode == 0 ? gemm_mfma_t<true>(epi, A, lda, Wb, M, N, K, C, ldc, st)
-                     : gemm_mfma_t<false>(epi, A, lda, Wb, M, N, K, C, ldc, st);
+hipError_t launch_gemm(bool w_bf16, int epi, const ActBuf& A, int lda, const void* W, int M, int N,
+                       int K, float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
+  if (K % kBK) return hipErrorInvalidValue;
+  if (A.nt == 0) {
+#define WICI_F32(WT)                                                                            \
+  switch (epi) {                                                                                \
+    case GEMV_STORE: return gemm_f32<WT, GEMV_STORE>(A, lda, static_cast<const WT*>(W), M, N, K, C, ldc, H, ldh, st); \
+    case GEMV_RESID: return gemm_f32<WT, GEMV_RESID>(A, lda, static_cast<const WT*>(W), M, N, K, C, ldc, H, ldh, st); \
+    case GEMV_SWIGLU: return gemm_f32<WT, GEMV_SWIGLU>(A, lda, static_cast<const WT*>(W), M, N, K, C, ldc, H, ldh, st); \
+    default: return hipErrorInvalidValue;                                                       \
   }
-  if (w_bf16)
-    return gemm_f32_t<bf16_t>(epi, A, lda, static_cast<const bf16_t*>(W), M, N, K, C, ldc, st);
-  return gemm_f32_t<float>(epi, A, lda, static_cast<const float*>(W), M, N, K, C, ldc, st);
+    if (w_bf16) { WICI_F32(bf16_t) } else { WICI_F32(float) }
+#undef WICI_F32
+  }
+  if (!w_bf16) return hipErrorInvalidValue;
+  const bf16_t* Wb = static_cast<const bf16_t*>(W);
+  switch (epi) {
+    case GEMV_STORE: return gemm_mfma<GEMV_STORE>(A, lda, Wb, M, N, K, C, ldc, H, ldh, st);
+    case GEMV_RESID: return gemm_mfma<GEMV_RESID>(A, lda, Wb, M, N, K, C, ldc, H, ldh, st);
+    case GEMV_SWIGLU: return gemm_mfma<GEMV_SWIGLU>(A, lda, Wb, M, N, K, C, ldc, H, ldh, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace wici

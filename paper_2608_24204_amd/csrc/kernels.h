@@ -33,9 +33,9 @@ hipError_t launch_set_token(void* state, int token, hipStream_t st);
 hipError_t launch_reset_state(void* state, hipStream_t st);
 hipError_t launch_init_block_table(int32_t* table, int n_pages, hipStream_t st);
 
-// y[t, :] = RMSNorm(x[t, :]) * gain for T rows of width d.
+// y[t, :] = RMSNorm(x[t, :]) * gain for T rows of width d (row stride d).
 hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int T, int d,
-                               float* y, hipStream_t st);
+                               const ActBuf& y, hipStream_t st);
 
 struct KvLayout {
   void* base;            // this layer's pool
@@ -55,9 +55,9 @@ hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
                               hipStream_t st);
 
 // Prefill attention: queries = rotated q rows of qkv (T rows at p0..), keys =
-// cache positions [0, p0+T), causal; out [T, Hq*hd] fp32.
+// cache positions [0, p0+T), causal; out [T, Hq*hd] (row stride Hq*hd).
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
-                               KvLayout kv, float* out, hipStream_t st);
+                               KvLayout kv, const ActBuf& out, hipStream_t st);
 
 // Decode attention at position state->pos: rotates q and the new k, appends the
 // new k, v, attends over [0, pos] in splits of 64 positions (grid nsplit x Hkv,
@@ -69,12 +69,13 @@ hipError_t launch_attn_decode(bool kv_bf16, const float* qkv, int Hq, const floa
 int attn_decode_splits(int max_seq);
 bool attn_group_supported(int G);
 
-// C[M, N] (ldc) = A[M, K] (fp32, lda) x W[N, K]^T with epilogue as launch_gemv
-// (STORE / RESID / SWIGLU; SWIGLU writes C[M, N/2]).
-//   mode 0: MFMA bf16, A split into hi + lo bf16 terms
-//   mode 1: MFMA bf16, A rounded to bf16
-//   mode 2: vector fp32 (W bf16 or fp32)
-hipError_t launch_gemm(int mode, bool w_bf16, int epi, const float* A, int lda, const void* W,
-                       int M, int N, int K, float* C, int ldc, hipStream_t st);
+// C[M, N] (ldc) = A[M, K] (lda) x W[N, K]^T with epilogue STORE / RESID (into C,
+// fp32) or SWIGLU (H[M, N/2] (ldh) = silu(gate) * up of the packed column pairs,
+// written as an activation buffer).  A.nt == 0: vector fp32 product (W bf16 or
+// fp32); A.nt = 1..3: matrix-core product of the nt bf16 planes with bf16 W.
+// K must be a multiple of 32.
+hipError_t launch_gemm(bool w_bf16, int epi, const ActBuf& A, int lda, const void* W, int M,
+                       int N, int K, float* C, int ldc, const ActBuf& H, int ldh,
+                       hipStream_t st);
 
 }  // namespace wici

@@ -73,10 +73,10 @@ hipError_t launch_init_block_table(int32_t* table, int n_pages, hipStream_t st) 
 // ---- RMSNorm of T rows ------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_rmsnorm_rows(const float* __restrict__ x,
                                                       const float* __restrict__ g, float eps,
-                                                      int d, float* __restrict__ y) {
+                                                      int d, ActBuf y) {
   __shared__ float red[4];
   const float* xr = x + (size_t)blockIdx.x * d;
-  float* yr = y + (size_t)blockIdx.x * d;
+  const size_t yr = (size_t)blockIdx.x * d;
   float ss = 0.f;
   for (int k = threadIdx.x * 4; k < d; k += 1024) {
     const float4 v = *reinterpret_cast<const float4*>(xr + k);
@@ -84,15 +84,17 @@ __global__ __launch_bounds__(256) void k_rmsnorm_rows(const float* __restrict__ 
   }
   const float r = 1.0f / sqrtf(block256_sum(ss, red) / (float)d + eps);
   for (int k = threadIdx.x * 4; k < d; k += 1024) {
-    float4 v = *reinterpret_cast<const float4*>(xr + k);
+    const float4 v = *reinterpret_cast<const float4*>(xr + k);
     const float4 w = *reinterpret_cast<const float4*>(g + k);
-    v.x = v.x * r * w.x; v.y = v.y * r * w.y; v.z = v.z * r * w.z; v.w = v.w * r * w.w;
-    *reinterpret_cast<float4*>(yr + k) = v;
+    store_act(y, yr + k + 0, v.x * r * w.x);
+    store_act(y, yr + k + 1, v.y * r * w.y);
+    store_act(y, yr + k + 2, v.z * r * w.z);
+    store_act(y, yr + k + 3, v.w * r * w.w);
   }
 }
 
 hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int T, int d,
-                               float* y, hipStream_t st) {
+                               const ActBuf& y, hipStream_t st) {
   hipLaunchKernelGGL(k_rmsnorm_rows, dim3(T), dim3(256), 0, st, x, gain, eps, d, y);
   return hipGetLastError();
 }

@@ -61,7 +61,7 @@ bool config_ok(const wici_config* c, std::string* why) {
   if (c->prefill_chunk < 1 || c->prefill_chunk > 8192) return bad("prefill_chunk out of range");
   if (c->kv_page != 16 && c->kv_page != 32 && c->kv_page != 64 && c->kv_page != 128)
     return bad("kv_page must be 16, 32, 64 or 128");
-  if (c->prefill_mode < WICI_PREFILL_BF16X2 || c->prefill_mode > WICI_PREFILL_F32)
+  if (c->prefill_mode < WICI_PREFILL_BF16X2 || c->prefill_mode > WICI_PREFILL_BF16X3)
     return bad("bad prefill_mode");
   if (c->weight_dtype == WICI_F32 && c->prefill_mode != WICI_PREFILL_F32)
     return bad("fp32 weights need prefill_mode WICI_PREFILL_F32");
@@ -104,11 +104,12 @@ Layout make_layout(const wici_config& c) {
   L.nsplit = wici::attn_decode_splits(c.max_seq);
   const size_t C = c.prefill_chunk;
   o = 0;
+  // activation buffers hold fp32 rows or up to three bf16 planes (6 bytes/value)
   L.x = o; o = align_up(o + C * d * 4);
-  L.a = o; o = align_up(o + C * d * 4);
+  L.a = o; o = align_up(o + C * d * 6);
   L.qkv = o; o = align_up(o + C * nqkv * 4);
-  L.att = o; o = align_up(o + C * qd * 4);
-  L.h = o; o = align_up(o + C * F * 4);
+  L.att = o; o = align_up(o + C * qd * 6);
+  L.h = o; o = align_up(o + C * F * 6);
   L.logits = o; o = align_up(o + V * 4);
   L.parts = o; o = align_up(o + kMaxGemvBlocks * sizeof(ArgmaxPart));
   L.part_o = o; o = align_up(o + (size_t)c.n_heads * L.nsplit * c.head_dim * 4);
@@ -283,12 +284,22 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   const bool wb = c.weight_dtype == WICI_BF16, kb = c.kv_dtype == WICI_BF16;
   const int d = c.d_model, F = c.ffn_dim, qd = c.n_heads * c.head_dim;
   const int nqkv = qd + 2 * c.n_kv_heads * c.head_dim;
-  const int mode = c.prefill_mode;
   float* x = m->S<float>(L.x);
-  float* a = m->S<float>(L.a);
   float* qkv = m->S<float>(L.qkv);
-  float* att = m->S<float>(L.att);
-  float* h = m->S<float>(L.h);
+  const size_t C = c.prefill_chunk;
+  const int nt = c.prefill_mode == WICI_PREFILL_F32 ? 0
+                 : c.prefill_mode == WICI_PREFILL_BF16 ? 1
+                 : c.prefill_mode == WICI_PREFILL_BF16X2 ? 2 : 3;
+  auto act = [&](size_t off, size_t width) {
+    wici::ActBuf b;
+    b.f32 = m->S<float>(off);
+    b.planes = m->S<wici::bf16_t>(off);
+    b.plane_stride = C * width;
+    b.nt = nt;
+    return b;
+  };
+  const wici::ActBuf a = act(L.a, d), att = act(L.att, qd), h = act(L.h, F);
+  const wici::ActBuf none{};
   hipStream_t s = m->stream;
   hipError_t e;
   if ((e = wici::launch_embed(wb, m->dw + L.embed, d, m->S<int32_t>(L.tokens), T, nullptr, x, s)))
@@ -297,24 +308,24 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
     if ((e = wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, T, d,
                                        a, s)))
       return e;
-    if ((e = wici::launch_gemm(mode, wb, wici::GEMV_STORE, a, d, m->dw + m->layer(l, L.l_wqkv), T,
-                               nqkv, d, qkv, nqkv, s)))
+    if ((e = wici::launch_gemm(wb, wici::GEMV_STORE, a, d, m->dw + m->layer(l, L.l_wqkv), T,
+                               nqkv, d, qkv, nqkv, none, 0, s)))
       return e;
     if ((e = wici::launch_rope_append(kb, qkv, T, p0, c.n_heads, m->W<float>(L.rope_cos),
                                       m->W<float>(L.rope_sin), m->kv(l), s)))
       return e;
     if ((e = wici::launch_attn_prefill(kb, qkv, T, p0, c.n_heads, m->kv(l), att, s))) return e;
-    if ((e = wici::launch_gemm(mode, wb, wici::GEMV_RESID, att, qd, m->dw + m->layer(l, L.l_wo), T,
-                               d, qd, x, d, s)))
+    if ((e = wici::launch_gemm(wb, wici::GEMV_RESID, att, qd, m->dw + m->layer(l, L.l_wo), T, d,
+                               qd, x, d, none, 0, s)))
       return e;
     if ((e = wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_fnorm)), c.rms_eps, T, d,
                                        a, s)))
       return e;
-    if ((e = wici::launch_gemm(mode, wb, wici::GEMV_SWIGLU, a, d, m->dw + m->layer(l, L.l_wgu), T,
-                               2 * F, d, h, F, s)))
+    if ((e = wici::launch_gemm(wb, wici::GEMV_SWIGLU, a, d, m->dw + m->layer(l, L.l_wgu), T,
+                               2 * F, d, nullptr, 0, h, F, s)))
       return e;
-    if ((e = wici::launch_gemm(mode, wb, wici::GEMV_RESID, h, F, m->dw + m->layer(l, L.l_wdown), T,
-                               d, F, x, d, s)))
+    if ((e = wici::launch_gemm(wb, wici::GEMV_RESID, h, F, m->dw + m->layer(l, L.l_wdown), T, d, F,
+                               x, d, none, 0, s)))
       return e;
   }
   return hipSuccess;

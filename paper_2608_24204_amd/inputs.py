@@ -137,3 +137,24 @@ def weights_f64(cfg: ModelConfig, weights: dict[str, np.ndarray],
         threads = min(16, os.cpu_count() or 1)
     with ThreadPoolExecutor(max(1, threads)) as ex:
         return dict(ex.map(conv, weights.items()))
+
+
+class LazyF64:
+    """Read-only mapping name -> float64 array that widens the stored weight on
+    each access (nothing is cached), so a float64 forward over a model that is too
+    large to hold in float64 touches one matrix at a time."""
+
+    def __init__(self, weights: dict[str, np.ndarray]):
+        self._w = weights
+
+    def __getitem__(self, name: str) -> np.ndarray:
+        a = self._w[name]
+        if a.dtype == np.uint16:
+            return bf16_bits_to_f32(a).astype(np.float64)
+        return a.astype(np.float64)
+
+    def __contains__(self, name: str) -> bool:
+        return name in self._w
+
+    def keys(self):
+        return self._w.keys()

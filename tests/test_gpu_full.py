@@ -1,0 +1,65 @@
+"""Full-size parity: a whole greedy request of a workload configuration (its real
+shapes, prompt length and decode steps, the launch configuration the benchmark
+times) on the GPU, against the float64 oracle's logits at every generated step
+(the oracle runs once over prompt + generated ids with all positions' logits, so
+each step is teacher-forced on the GPU's own ids).
+
+The 1B- and 8B-shaped configurations run by default; the long-context 8B and the
+32B shapes (minutes of float64 host work each) run when WICI_FULL_PARITY=all."""
+
+from __future__ import annotations
+
+import json
+import os
+import time
+
+import numpy as np
+import pytest
+
+from oracle import DecoderOracle
+from paper_2608_24204_amd import configs, inputs
+from tests.parity import compare
+
+pytestmark = pytest.mark.gpu
+
+DEFAULT = ["1b", "8b"]
+OPT_IN = ["8b_long", "32b"]
+SELECTED = DEFAULT + (OPT_IN if os.environ.get("WICI_FULL_PARITY") == "all" else [])
+MODES = os.environ.get("WICI_FULL_PARITY_MODES", "bf16x3").split(",")
+
+
+def _report_path():
+    d = os.path.join(os.environ.get("GRAFT_REPO_ROOT", "."), "gpurun_out")
+    os.makedirs(d, exist_ok=True)
+    return os.path.join(d, "full_parity.jsonl")
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("name", DEFAULT + OPT_IN)
+def test_full_size_greedy_run_matches_oracle(cuda_ok, name, mode):
+    if name not in SELECTED:
+        pytest.skip("long float64 oracle run; set WICI_FULL_PARITY=all")
+    from paper_2608_24204_amd.binding import WiciModel
+    cfg = configs.CONFIGS[name]
+    t0 = time.time()
+    w = inputs.make_weights(cfg)
+    prompt = inputs.make_prompt(cfg)
+    m = WiciModel(cfg, prefill_mode=mode)
+    try:
+        m.load_weights(w)
+        ids, logs = m.generate(prompt, cfg.decode_steps, want_logits=True)
+    finally:
+        m.close()
+    t1 = time.time()
+    seq = np.concatenate([prompt, np.asarray(ids[:-1])])
+    orc = DecoderOracle(cfg, inputs.LazyF64(w), max_seq=len(seq))
+    ora = orc.forward(seq, all_logits=True, first_row=len(prompt) - 1)
+    t2 = time.time()
+    rep = compare(ids, logs, ora)
+    rec = {"config": name, "prefill_mode": mode, **rep.summary(),
+           "near_tie_steps": rep.near_ties[:10], "gpu_s": t1 - t0, "oracle_s": t2 - t1}
+    print("[full parity]", json.dumps(rec), flush=True)
+    with open(_report_path(), "a") as f:
+        f.write(json.dumps(rec) + "\n")
+    assert rep.max_rel_err <= 2e-2, rec
+    assert rep.strict_ids, rec

@@ -96,7 +96,7 @@ def test_ragged_prompts_chunks_and_pages(cuda_ok, P, chunk, page):
     assert rep.strict_ids, rep.summary()
 
 
-@pytest.mark.parametrize("mode", ["bf16x2", "bf16", "f32"])
+@pytest.mark.parametrize("mode", ["bf16x3", "bf16x2", "bf16", "f32"])
 def test_prefill_modes(cuda_ok, mode):
     cfg = SMALL["gqa64_bf16"]
     prompt = inputs.make_prompt(cfg, 130)
