@@ -8,7 +8,8 @@
 // the same launch writes).  A second small kernel merges the splits.
 //
 // Prefill: one block per (64 queries, query head), keys streamed through LDS in
-// blocks of 64 with an online softmax, fp32 throughout.
+// blocks of 64 with an online softmax; on the matrix cores for a bf16 cache (the
+// fp32 query and probabilities split into bf16 terms), else fp32 vector code.
 #include "common.h"
 #include "kernels.h"
 
@@ -386,6 +387,213 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
   }
 }
 
+// ------------------------------------------------------------- prefill, MFMA
+// Flash attention on the matrix cores.  Block = 4 wavefronts = 64 query rows of
+// one query head (16 per wavefront); keys stream through LDS in blocks of 64
+// (K as [key][d], V transposed to [d][key]), the next block's loads in flight
+// while the current one is processed.  Per key block a wavefront computes
+// S^T = K Q^T (so each lane ends up with 16 keys of one query, the row layout the
+// A operand of the next product needs), the online-softmax update, and
+// O += P V.  The query and the probabilities are fp32 values split into NT bf16
+// terms (K and V are stored in bf16, hence exact), so both products keep the
+// precision of their fp32 operands.
+template <int HD, int NT>
+__global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restrict__ qkv, int T,
+                                                           int p0, int Hq, KvLayout kv,
+                                                           ActBuf out) {
+  constexpr int BQ = 64, BKEY = 64, KP = HD + 8, VP = BKEY + 8;
+  constexpr int DS = HD / 32;   // 32-deep steps over the head dimension
+  constexpr int DT = HD / 16;   // 16-wide output column tiles
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[BKEY][KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt[HD][VP];
+
+  const int qb = blockIdx.x * BQ, h = blockIdx.y;
+  const int Hkv = kv.n_kv, g = h / (Hq / Hkv);
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const int width = (Hq + 2 * Hkv) * HD;
+  const bf16_t* base = static_cast<const bf16_t*>(kv.base);
+  const size_t head_stride = (size_t)kv.page * HD;
+
+  // ---- this lane's query (B operand of S^T = K Q^T): row l16 of the wavefront ----
+  const int tq = qb + wave * 16 + l16;        // query row in the chunk
+  const bool qvalid = tq < T;
+  const int qpos = p0 + tq;
+  const float scale = 1.0f / sqrtf((float)HD);
+  bf16x8_t qf[NT][DS];
+  {
+    const float* qr = qkv + (size_t)(qvalid ? tq : 0) * width + (size_t)h * HD;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = qvalid ? qr[32 * s + 8 * lg + e] * scale : 0.f;
+#pragma unroll
+      for (int p = 0; p < NT; ++p) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const bf16_t t = f32_to_bf16(v[e]);
+          qf[p][s][e] = __builtin_bit_cast(__bf16, t);
+          v[e] -= bf16_to_f32(t);
+        }
+      }
+    }
+  }
+
+  // ---- key/value loading: thread -> (key pair, 16-wide column chunk) --------------
+  constexpr int NCH = HD / 16;                // column chunks per key
+  constexpr int PAIRS = BKEY / 2;
+  constexpr int ITEMS = PAIRS * NCH;          // (pair, chunk) items per block
+  constexpr int PER = (ITEMS + 255) / 256;
+  uint4 rk[PER][2][2], rv[PER][2][2];         // [item][key of pair][16-byte half]
+  const int kend = p0 + min(T, qb + BQ);      // keys [0, kend) are visible to this block
+  auto gload = [&](int kb) {
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int item = tid + it * 256;
+      if (item < ITEMS) {
+        const int pr = item / NCH, ch = item % NCH;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int j = kb + 2 * pr + u;
+          if (j < kend) {
+            const int pp = kv.table[j / kv.page];
+            const bf16_t* kp = base + (((size_t)pp * 2 + 0) * Hkv + g) * head_stride +
+                               (size_t)(j % kv.page) * HD + ch * 16;
+            const bf16_t* vp = kp + (size_t)Hkv * head_stride;
+            rk[it][u][0] = *reinterpret_cast<const uint4*>(kp);
+            rk[it][u][1] = *reinterpret_cast<const uint4*>(kp + 8);
+            rv[it][u][0] = *reinterpret_cast<const uint4*>(vp);
+            rv[it][u][1] = *reinterpret_cast<const uint4*>(vp + 8);
+          } else {
+            rk[it][u][0] = rk[it][u][1] = rv[it][u][0] = rv[it][u][1] = make_uint4(0, 0, 0, 0);
+          }
+        }
+      }
+    }
+  };
+  auto sstore = [&]() {
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int item = tid + it * 256;
+      if (item < ITEMS) {
+        const int pr = item / NCH, ch = item % NCH;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          *reinterpret_cast<uint4*>(&Ks[2 * pr + u][ch * 16]) = rk[it][u][0];
+          *reinterpret_cast<uint4*>(&Ks[2 * pr + u][ch * 16 + 8]) = rk[it][u][1];
+        }
+        // V transposed: column d of the pair's two keys packed in one dword
+        const uint32_t* a = reinterpret_cast<const uint32_t*>(&rv[it][0][0]);
+        const uint32_t* b = reinterpret_cast<const uint32_t*>(&rv[it][1][0]);
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          const uint32_t x0 = a[w], x1 = b[w];
+          // elements 2w, 2w+1 of the chunk
+          *reinterpret_cast<uint32_t*>(&Vt[ch * 16 + 2 * w][2 * pr]) = (x0 & 0xffffu) | (x1 << 16);
+          *reinterpret_cast<uint32_t*>(&Vt[ch * 16 + 2 * w + 1][2 * pr]) = (x0 >> 16) | (x1 & 0xffff0000u);
+        }
+      }
+    }
+  };
+
+  floatx4_t o[DT];
+#pragma unroll
+  for (int u = 0; u < DT; ++u) o[u] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_part = 0.f;
+
+  gload(0);
+  for (int kb = 0; kb < kend; kb += BKEY) {
+    __syncthreads();          // previous block's readers are done with LDS
+    sstore();
+    __syncthreads();
+    if (kb + BKEY < kend) gload(kb + BKEY);
+
+    // S^T tile t: lane holds S[query l16][key 16 t + 4 lg + r]
+    floatx4_t st[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      st[t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < DS; ++s) {
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(&Ks[16 * t + l16][32 * s + 8 * lg]);
+#pragma unroll
+        for (int p = 0; p < NT; ++p)
+          st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[p][s], st[t], 0, 0, 0);
+      }
+    }
+    // causal mask, block max
+    float bm = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = kb + 16 * t + 4 * lg + r;
+        if (j > qpos || j >= kend) st[t][r] = -INFINITY;
+        bm = fmaxf(bm, st[t][r]);
+      }
+    bm = fmaxf(bm, __shfl_xor(bm, 16));
+    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    const float m_new = fmaxf(m_run, bm);
+    const float corr = m_new == -INFINITY ? 1.f : __expf(m_run - m_new);
+    m_run = m_new;
+    l_part *= corr;
+    // probabilities, split into NT bf16 terms in the A-operand key order
+    bf16x8_t pf[NT][2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float sv = st[2 * c + (e >> 2)][e & 3];
+        float pv = sv == -INFINITY ? 0.f : __expf(sv - m_new);
+        l_part += pv;
+#pragma unroll
+        for (int p = 0; p < NT; ++p) {
+          const bf16_t tb = f32_to_bf16(pv);
+          pf[p][c][e] = __builtin_bit_cast(__bf16, tb);
+          pv -= bf16_to_f32(tb);
+        }
+      }
+    // rescale the output rows (queries 4 lg + r) by their correction factors
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float cr = __shfl(corr, 4 * lg + r);
+#pragma unroll
+      for (int u = 0; u < DT; ++u) o[u][r] *= cr;
+    }
+    // O += P V: B operand = V^T rows d, keys in the same slot order as P
+#pragma unroll
+    for (int u = 0; u < DT; ++u) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const bf16_t* vr = &Vt[16 * u + l16][32 * c + 4 * lg];
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+        const uint4 w4 = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, w4);
+#pragma unroll
+        for (int p = 0; p < NT; ++p)
+          o[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf[p][c], vf, o[u], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- normalise and write: lane holds O[query 4 lg + r][d 16 u + l16] -----------
+  float l_tot = l_part + __shfl_xor(l_part, 16);
+  l_tot += __shfl_xor(l_tot, 32);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int qrow = 4 * lg + r;
+    const float inv = 1.0f / __shfl(l_tot, qrow);
+    const int t = qb + wave * 16 + qrow;
+    if (t < T) {
+      const size_t ob = (size_t)t * Hq * HD + (size_t)h * HD;
+#pragma unroll
+      for (int u = 0; u < DT; ++u) store_act(out, ob + 16 * u + l16, o[u][r] * inv);
+    }
+  }
+}
+
 template <int HD, typename KT>
 static hipError_t attn_prefill_t(const float* qkv, int T, int p0, int Hq, KvLayout kv,
                                  const ActBuf& out, hipStream_t s) {
@@ -394,8 +602,29 @@ static hipError_t attn_prefill_t(const float* qkv, int T, int p0, int Hq, KvLayo
   return hipGetLastError();
 }
 
+template <int HD>
+static hipError_t attn_prefill_mfma(const float* qkv, int T, int p0, int Hq, KvLayout kv,
+                                    const ActBuf& out, hipStream_t s) {
+  const dim3 grid((T + 63) / 64, Hq);
+  switch (out.nt) {
+    case 1: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 1>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
+    case 2: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 2>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
+    case 3: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 3>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// bf16 cache with split-activation output: matrix cores, with the query and the
+// probabilities carried in as many bf16 terms as the output; otherwise the fp32
+// vector kernel.
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
                                KvLayout kv, const ActBuf& out, hipStream_t s) {
+  if (kv_bf16 && out.nt >= 1) {
+    if (kv.hd == 128) return attn_prefill_mfma<128>(qkv, T, p0, Hq, kv, out, s);
+    if (kv.hd == 64) return attn_prefill_mfma<64>(qkv, T, p0, Hq, kv, out, s);
+    return hipErrorInvalidValue;
+  }
   if (kv.hd == 128) {
     if (kv_bf16) return attn_prefill_t<128, bf16_t>(qkv, T, p0, Hq, kv, out, s);
     return attn_prefill_t<128, float>(qkv, T, p0, Hq, kv, out, s);
