@@ -167,10 +167,12 @@ class DecoderOracle:
     def _lm_weight(self) -> np.ndarray:
         return self.w["tok_embeddings"] if self.cfg.tied_embeddings else self.w["lm_head"]
 
-    def forward(self, tokens, all_logits: bool = False, first_row: int = 0) -> np.ndarray:
+    def forward(self, tokens, all_logits: bool = False, first_row: int = 0,
+                progress=None) -> np.ndarray:
         """Append ``tokens`` at the current position; return the logits of the last
         appended position ([vocab]) or, with all_logits, of appended rows
-        first_row.. ([T - first_row, vocab])."""
+        first_row.. ([T - first_row, vocab]).  ``progress(layer)`` is called after
+        each layer (long runs report liveness through it)."""
         c = self.cfg
         tokens = np.asarray(tokens, dtype=np.int64).reshape(-1)
         T = tokens.size
@@ -199,6 +201,8 @@ class DecoderOracle:
             wn = rms_norm(x, self.w[pre + "ffn_norm"], c.rms_eps)
             h = silu(wn @ self.w[pre + "w_gate"].T) * (wn @ self.w[pre + "w_up"].T)
             x = x + h @ self.w[pre + "w_down"].T
+            if progress is not None:
+                progress(l)
         self.pos = p0 + T
         rows = x[first_row:] if all_logits else x[-1:]
         logits = rms_norm(rows, self.w["norm"], c.rms_eps) @ self._lm_weight().T

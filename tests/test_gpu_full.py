@@ -53,7 +53,12 @@ def test_full_size_greedy_run_matches_oracle(cuda_ok, name, mode):
     t1 = time.time()
     seq = np.concatenate([prompt, np.asarray(ids[:-1])])
     orc = DecoderOracle(cfg, inputs.LazyF64(w), max_seq=len(seq))
-    ora = orc.forward(seq, all_logits=True, first_row=len(prompt) - 1)
+    print(f"[full parity] {name}: GPU run done in {t1 - t0:.1f} s; oracle over {len(seq)} "
+          f"positions", flush=True)
+    ora = orc.forward(seq, all_logits=True, first_row=len(prompt) - 1,
+                      progress=lambda l: print(f"[full parity] {name}: oracle layer {l + 1}/"
+                                               f"{cfg.n_layers} ({time.time() - t1:.0f} s)",
+                                               flush=True))
     t2 = time.time()
     rep = compare(ids, logs, ora)
     rec = {"config": name, "prefill_mode": mode, **rep.summary(),
