@@ -47,6 +47,24 @@ def gateup_bytes(cfg) -> int:
     return 2 * cfg.ffn_dim * cfg.d_model * cfg.wbytes + 2 * cfg.d_model * 4 + cfg.ffn_dim * 4
 
 
+def measured_traffic(cfg):
+    """HBM bytes per gate/up GEMV launch from the committed memory-counter summary,
+    if it was taken on this workload with the current kernel source; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"traffic_gemv_gateup_{cfg.name}.md")
+    src = os.path.join(ROOT, "paper_2608_24204_amd", "csrc", "gemv.hip")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    want = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if f"gemv.hip: {want}" not in text:
+        return None
+    for line in text.splitlines():
+        if line.startswith("traffic_bytes_per_launch gateup:"):
+            return int(line.split(":")[1])
+    return None
+
+
 def profile_pass(model, cfg, prompt, n_decode):
     """Eager decode steps with HIP events around every launch (same positions as a
     timed request).  Returns mean per-launch ms per kernel class and per-token sums."""
@@ -112,6 +130,9 @@ def main(argv=None):
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--cpu-prompt", type=int, default=128)
     ap.add_argument("--cpu-decode", type=int, default=3)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="before the timed region, copy MIB MiB device-to-device (a plain "
+                         "copy of known size, for calibrating memory counters)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -134,6 +155,16 @@ def main(argv=None):
     model.load_weights(w)
     log(f"weights uploaded in {time.perf_counter() - t0:.1f} s")
 
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.calibrate_copy} MiB done")
+        del src, dst
     for i in range(args.warmup):
         ttft, dec, _ = run_request(model, prompt, n_decode)
         log(f"warmup {i}: ttft {ttft * 1e3:.2f} ms, decode {n_decode / dec:.1f} tok/s")
@@ -178,7 +209,7 @@ def main(argv=None):
         ach = gu / (mean["gateup"] / 1e3)
         res["roofline"] = {"kernel": "k_gemv gate/up (+RMSNorm prologue, SwiGLU epilogue)",
                            "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9,
-                           "unit": "GB/s", "frac": ach / HBM_PEAK, "traffic": None,
+                           "unit": "GB/s", "frac": ach / HBM_PEAK, "traffic": measured_traffic(cfg),
                            "bytes_per_launch": gu, "avg_launch_ms": mean["gateup"],
                            "method": "HIP events around each launch, eager profiling pass over "
                                      "one request's decode steps"}
