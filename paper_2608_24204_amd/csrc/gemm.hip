@@ -222,14 +222,13 @@ static hipError_t gemm_mfma_launch(const ActBuf& A, int lda, const bf16_t* W, in
   return hipGetLastError();
 }
 
-// Block shape: 256 x 128 when that still gives every CU a tile (fewer re-reads of
-// the weights), else 128 x 128.
+// Block shape 128 x 128 (four waves of 64 x 64).  Measured on the projection
+// shapes of 1B-32B models at 1-2K rows, it beats 256 x 128 blocks by 14-35%: the
+// smaller block keeps two workgroups resident per CU, which hides the global-load
+// latency of the next K slice better than the halved weight re-reads save.
 template <int NT, int EPI>
 static hipError_t gemm_mfma_nt(const ActBuf& A, int lda, const bf16_t* W, int M, int N, int K,
                                float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
-  const long big_tiles = (long)((M + 255) / 256) * ((N + 127) / 128);
-  if (big_tiles >= 256)
-    return gemm_mfma_launch<NT, 4, 2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
   return gemm_mfma_launch<NT, 2, 2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
 }
 
