@@ -30,13 +30,18 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def run_request(model, prompt, n_decode):
+def run_request(model, prompt, n_decode, device_resident=False):
+    """One request: reset, prefill (TTFT), n_decode greedy steps, either one
+    wici_decode_step call per token or one wici_decode_n call for all of them."""
     model.reset_kv()
     t0 = time.perf_counter()
     tok, _ = model.prefill(prompt)
     t1 = time.perf_counter()
-    for _ in range(n_decode):
-        model.decode_step(-1)
+    if device_resident:
+        model.decode_n(n_decode)
+    else:
+        for _ in range(n_decode):
+            model.decode_step(-1)
     t2 = time.perf_counter()
     return t1 - t0, t2 - t1, tok
 
@@ -178,6 +183,13 @@ def main(argv=None):
         log(f"step {i}: ttft {ttft * 1e3:.2f} ms, decode {n_decode / dec:.1f} tok/s")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
+    # the same requests with the decode steps in one device-resident call
+    dn = []
+    for i in range(args.steps):
+        _, dec, _ = run_request(model, prompt, n_decode, device_resident=True)
+        dn.append(dec)
+    torch.cuda.synchronize()
+    log(f"wici_decode_n: {n_decode * args.steps / sum(dn):.1f} tok/s")
 
     decode_tok_s = n_decode * args.steps / sum(decs)
     ttft_ms = float(np.median(ttfts)) * 1e3
@@ -200,6 +212,8 @@ def main(argv=None):
         "prefill_flops": pf_flops,
         "prefill_mfma_frac": pf_flops / (ttft_ms / 1e3) / MFMA_BF16_PEAK,
         "prefill_mode": args.prefill_mode or ("f32" if cfg.weight_dtype == "f32" else "bf16x3"),
+        "decode_n_tok_s": n_decode * args.steps / sum(dn),
+        "decode_n_hbm_frac": bytes_tok * n_decode * args.steps / sum(dn) / HBM_PEAK,
     }
 
     if not args.no_profile:

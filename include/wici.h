@@ -153,6 +153,25 @@ wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
 wici_status wici_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
                              float* logits);
 
+/* n greedy decode steps without a host round trip per token: the on-GPU form of
+ * the paper's function batching, several calls answered in one round trip
+ * (Sec. "Batching and Trace Replay"), applied to the per-token call group that
+ * the paper replays as a trace.  Each step's argmax stays on the device and is
+ * the next step's input; the captured step graph is replayed n times back to
+ * back and the host waits once.  token_in as for wici_decode_step (< 0: the
+ * last returned token).  tokens_out (host array, n entries) receives the n
+ * generated tokens in order; *n_done the number that are valid.  logits (host,
+ * [vocab], may be NULL) receives the last step's fp32 logits.  Results are
+ * bit-identical to n calls of wici_decode_step.  Synchronous.
+ * Errors: WICI_E_ARG (NULL tokens_out/n_done, n < 1, token_in >= vocab),
+ * WICI_E_STATE (no prefill since the last reset, or no token to feed),
+ * WICI_E_CAPACITY (position + n > max_seq; nothing is run), WICI_E_NUMERIC (a
+ * step's logits were not finite: the steps before it are returned in
+ * tokens_out[0 .. *n_done), the failed step's position was appended, the rest
+ * are -1 and ran as no-ops; the next decode call needs an explicit token_in). */
+wici_status wici_decode_n(wici_model* m, int32_t token_in, int32_t n, int32_t* tokens_out,
+                          int32_t* n_done, float* logits);
+
 /* Forget the sequence: position 0, KV pages returned to the pool.  Weights stay. */
 wici_status wici_reset_kv(wici_model* m);
 

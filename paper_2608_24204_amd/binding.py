@@ -27,7 +27,7 @@ WICI_FLAG_NO_GRAPH = 1
 
 # every entry point include/wici.h declares
 EXPORTED = ["wici_create", "wici_memory_requirements", "wici_bind_memory", "wici_load_weights",
-            "wici_prefill", "wici_decode_step", "wici_reset_kv", "wici_position",
+            "wici_prefill", "wici_decode_step", "wici_decode_n", "wici_reset_kv", "wici_position",
             "wici_read_kv", "wici_profile_decode_step", "wici_last_error", "wici_destroy"]
 
 
@@ -77,6 +77,7 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
         "wici_load_weights": ([P, ctypes.POINTER(WiciTensor), i32], ctypes.c_int),
         "wici_prefill": ([P, P, i32, ctypes.POINTER(i32), P], ctypes.c_int),
         "wici_decode_step": ([P, i32, ctypes.POINTER(i32), P], ctypes.c_int),
+        "wici_decode_n": ([P, i32, i32, P, ctypes.POINTER(i32), P], ctypes.c_int),
         "wici_reset_kv": ([P], ctypes.c_int),
         "wici_position": ([P, ctypes.POINTER(i32)], ctypes.c_int),
         "wici_read_kv": ([P, i32, i32, i32, P, P], ctypes.c_int),
@@ -217,6 +218,22 @@ class WiciModel:
         self._check(self.lib.wici_decode_step(self.h, int(token_in), ctypes.byref(out), lg),
                     "wici_decode_step")
         return out.value, (self._logits.copy() if want_logits else None)
+
+    def decode_n(self, n: int, token_in: int = -1, want_logits: bool = False):
+        """n greedy decode steps in one call (argmax fed back on the device).
+        Returns (int32 array of n tokens, last step's logits or None).  On non-finite
+        logits raises WiciError carrying `.tokens`, the steps that completed."""
+        toks = np.full(max(int(n), 1), -1, np.int32)
+        done = ctypes.c_int32()
+        lg = self._logits.ctypes.data if want_logits else None
+        st = self.lib.wici_decode_n(self.h, int(token_in), int(n), toks.ctypes.data,
+                                    ctypes.byref(done), lg)
+        if st == WICI_E_NUMERIC:
+            err = WiciError(st, f"wici_decode_n: {self.lib.wici_last_error(self.h).decode()}")
+            err.tokens = toks[:done.value].copy()
+            raise err
+        self._check(st, "wici_decode_n")
+        return toks[:n], (self._logits.copy() if want_logits else None)
 
     def reset_kv(self) -> None:
         self._check(self.lib.wici_reset_kv(self.h), "wici_reset_kv")

@@ -22,13 +22,18 @@ int gemv_argmax_blocks(int N);
 
 // Final argmax over `n` partials -> st->token; st->pos += advance (or = set_pos
 // when set_pos >= 0); st->bad set when a partial carries index -1 (a logit was
-// not finite), in which case st->token = -1.
-hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int advance,
-                               int set_pos, hipStream_t st);
+// not finite), in which case st->token = -1.  The chosen token is also stored
+// at hist[new pos - 1] (the token that follows that position).  A decode step
+// (advance > 0) that finds st->bad already set changes nothing: once a step of
+// a device-resident run has failed, the steps queued after it are no-ops.
+hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int32_t* hist,
+                               int advance, int set_pos, hipStream_t st);
 
-// x[t, :] = E[tokens[t], :] for t < T (tokens == nullptr: the state's token, T = 1).
+// x[t, :] = E[tokens[t], :] for t < T (tokens == nullptr: the state's token, T = 1;
+// a negative state token, left by a failed step, gives a zero row).
 hipError_t launch_embed(bool w_bf16, const void* E, int d, const int32_t* tokens, int T,
                         const void* state, float* x, hipStream_t st);
+// st->token = token and clear st->bad (a host-given token restarts decoding).
 hipError_t launch_set_token(void* state, int token, hipStream_t st);
 hipError_t launch_reset_state(void* state, hipStream_t st);
 hipError_t launch_init_block_table(int32_t* table, int n_pages, hipStream_t st);

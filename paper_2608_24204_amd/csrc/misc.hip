@@ -14,10 +14,13 @@ __global__ __launch_bounds__(256) void k_embed(const WT* __restrict__ E, int d,
                                                float* __restrict__ x) {
   const int t = blockIdx.x;
   const int tok = tokens ? tokens[t] : st->token;
-  const WT* row = E + (size_t)tok * d;
+  const WT* row = E + (size_t)(tok < 0 ? 0 : tok) * d;
   for (int k = threadIdx.x * 8; k < d; k += 256 * 8) {
     float v[8];
     load8(row + k, v);
+    if (tok < 0)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = 0.f;
     float4* o = reinterpret_cast<float4*>(x + (size_t)t * d + k);
     o[0] = make_float4(v[0], v[1], v[2], v[3]);
     o[1] = make_float4(v[4], v[5], v[6], v[7]);
@@ -36,7 +39,10 @@ hipError_t launch_embed(bool w_bf16, const void* E, int d, const int32_t* tokens
   return hipGetLastError();
 }
 
-__global__ void k_set_token(DecodeState* st, int token) { st->token = token; }
+__global__ void k_set_token(DecodeState* st, int token) {
+  st->token = token;
+  st->bad = 0;
+}
 
 __global__ void k_reset_state(DecodeState* st) {
   st->pos = 0;
@@ -151,7 +157,8 @@ hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
 
 // ---- argmax, second pass -------------------------------------------------------------
 __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restrict__ part,
-                                                        int n, DecodeState* st, int advance,
+                                                        int n, DecodeState* st,
+                                                        int32_t* __restrict__ hist, int advance,
                                                         int set_pos) {
   __shared__ float sv[16];
   __shared__ int si[16];
@@ -179,16 +186,20 @@ __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restr
       if (am_better(sv[k], si[k], bv, bi)) { bv = sv[k]; bi = si[k]; }
       bad |= sbad[k];
     }
+    if (set_pos < 0 && st->bad) return;  // an earlier step of this run failed
+    const int pos = set_pos >= 0 ? set_pos : st->pos + advance;
+    const int tok = bad ? -1 : bi;
     st->bad = bad;
-    st->token = bad ? -1 : bi;
-    st->pos = set_pos >= 0 ? set_pos : st->pos + advance;
+    st->token = tok;
+    st->pos = pos;
+    if (pos >= 1) hist[pos - 1] = tok;
   }
 }
 
-hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int advance,
-                               int set_pos, hipStream_t st) {
+hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int32_t* hist,
+                               int advance, int set_pos, hipStream_t st) {
   hipLaunchKernelGGL(k_argmax_final, dim3(1), dim3(1024), 0, st, part, n,
-                     static_cast<DecodeState*>(state), advance, set_pos);
+                     static_cast<DecodeState*>(state), hist, advance, set_pos);
   return hipGetLastError();
 }
 

@@ -35,7 +35,8 @@ struct Layout {
   int n_pages;
   size_t kv_layer_stride, kv_bytes;
   // scratch
-  size_t x, a, qkv, att, h, logits, parts, part_o, part_ml, tokens, table, state, scratch_bytes;
+  size_t x, a, qkv, att, h, logits, parts, part_o, part_ml, tokens, table, state, hist;
+  size_t scratch_bytes;
   int nsplit;
 };
 
@@ -117,6 +118,7 @@ Layout make_layout(const wici_config& c) {
   L.tokens = o; o = align_up(o + C * 4);
   L.table = o; o = align_up(o + (size_t)L.n_pages * 4);
   L.state = o; o = align_up(o + sizeof(DecodeState));
+  L.hist = o; o = align_up(o + (size_t)c.max_seq * 4);  // token emitted after each position
   L.scratch_bytes = o;
   return L;
 }
@@ -271,7 +273,8 @@ hipError_t enqueue_decode(wici_model* m, std::vector<hipEvent_t>* marks = nullpt
   WICI_STEP(wici::launch_gemv(wb, wici::GEMV_ARGMAX, m->dw + L.lm_head, c.vocab, d, x,
                               m->W<float>(L.final_norm), c.rms_eps, m->S<float>(L.logits),
                               m->S<ArgmaxPart>(L.parts), &nb, s));
-  WICI_STEP(wici::launch_argmax_final(m->S<ArgmaxPart>(L.parts), nb, st, 1, -1, s));
+  WICI_STEP(wici::launch_argmax_final(m->S<ArgmaxPart>(L.parts), nb, st, m->S<int32_t>(L.hist), 1,
+                                      -1, s));
 #undef WICI_STEP
   return hipSuccess;
 }
@@ -346,6 +349,33 @@ wici_status finish_step(wici_model* m, int32_t* tok, float* logits) {
   *tok = m->h_state->token;
   m->have_token = true;
   return WICI_OK;
+}
+
+// Queue `n` decode steps: replays of the captured step graph (captured on first
+// use), or eager launches when graphs are off or the stream is the null stream.
+hipError_t launch_decode_steps(wici_model* m, int n) {
+  const bool use_graph = m->stream != nullptr && !(m->cfg.flags & WICI_FLAG_NO_GRAPH);
+  if (!use_graph) {
+    for (int i = 0; i < n; ++i)
+      if (hipError_t e = enqueue_decode(m)) return e;
+    return hipSuccess;
+  }
+  if (!m->gexec) {
+    if (hipError_t e = hipStreamBeginCapture(m->stream, hipStreamCaptureModeThreadLocal)) return e;
+    const hipError_t e = enqueue_decode(m);
+    hipGraph_t g = nullptr;
+    const hipError_t e2 = hipStreamEndCapture(m->stream, &g);
+    if (e != hipSuccess) {
+      if (g) (void)hipGraphDestroy(g);
+      return e;
+    }
+    if (e2 != hipSuccess) return e2;
+    m->graph = g;
+    if (hipError_t e3 = hipGraphInstantiate(&m->gexec, m->graph, nullptr, nullptr, 0)) return e3;
+  }
+  for (int i = 0; i < n; ++i)
+    if (hipError_t e = hipGraphLaunch(m->gexec, m->stream)) return e;
+  return hipSuccess;
 }
 
 }  // namespace
@@ -509,8 +539,8 @@ wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
                                m->S<float>(L.x) + (size_t)(last_T - 1) * c.d_model,
                                m->W<float>(L.final_norm), c.rms_eps, m->S<float>(L.logits),
                                m->S<ArgmaxPart>(L.parts), &nb, m->stream));
-  HIP_TRY(m, wici::launch_argmax_final(m->S<ArgmaxPart>(L.parts), nb, m->ds + L.state, 0,
-                                       m->pos + n_tokens, m->stream));
+  HIP_TRY(m, wici::launch_argmax_final(m->S<ArgmaxPart>(L.parts), nb, m->ds + L.state,
+                                       m->S<int32_t>(L.hist), 0, m->pos + n_tokens, m->stream));
   return finish_step(m, first_token, logits);
 }
 
@@ -525,23 +555,53 @@ wici_status wici_decode_step(wici_model* m, int32_t token_in, int32_t* next_toke
   if (m->pos + 1 > m->cfg.max_seq)
     return fail(m, WICI_E_CAPACITY, "position %d reached max_seq", m->pos);
   if (token_in >= 0) HIP_TRY(m, wici::launch_set_token(m->ds + m->L.state, token_in, m->stream));
-  const bool use_graph = m->stream != nullptr && !(m->cfg.flags & WICI_FLAG_NO_GRAPH);
-  if (use_graph) {
-    if (!m->gexec) {
-      HIP_TRY(m, hipStreamBeginCapture(m->stream, hipStreamCaptureModeThreadLocal));
-      const hipError_t e = enqueue_decode(m);
-      hipGraph_t g = nullptr;
-      const hipError_t e2 = hipStreamEndCapture(m->stream, &g);
-      HIP_TRY(m, e);
-      HIP_TRY(m, e2);
-      m->graph = g;
-      HIP_TRY(m, hipGraphInstantiate(&m->gexec, m->graph, nullptr, nullptr, 0));
-    }
-    HIP_TRY(m, hipGraphLaunch(m->gexec, m->stream));
-  } else {
-    HIP_TRY(m, enqueue_decode(m));
-  }
+  HIP_TRY(m, launch_decode_steps(m, 1));
   return finish_step(m, next_token, logits);
+}
+
+wici_status wici_decode_n(wici_model* m, int32_t token_in, int32_t n, int32_t* tokens_out,
+                          int32_t* n_done, float* logits) {
+  if (!m) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (!tokens_out || !n_done) return fail(m, WICI_E_ARG, "NULL tokens_out or n_done");
+  *n_done = 0;
+  if (n < 1) return fail(m, WICI_E_ARG, "n must be >= 1");
+  if (token_in >= m->cfg.vocab) return fail(m, WICI_E_ARG, "token id %d >= vocab", token_in);
+  if (!m->ready()) return fail(m, WICI_E_STATE, "weights not bound/loaded");
+  if (m->pos < 1) return fail(m, WICI_E_STATE, "decode before prefill");
+  if (token_in < 0 && !m->have_token) return fail(m, WICI_E_STATE, "no previous token to feed");
+  if ((int64_t)m->pos + n > m->cfg.max_seq)
+    return fail(m, WICI_E_CAPACITY, "position %d + %d steps exceeds max_seq %d", m->pos, n,
+                m->cfg.max_seq);
+  const int32_t pos0 = m->pos;
+  if (token_in >= 0) HIP_TRY(m, wici::launch_set_token(m->ds + m->L.state, token_in, m->stream));
+  HIP_TRY(m, launch_decode_steps(m, n));
+  // hist[pos0 .. pos0+n) holds the token emitted after each processed position
+  // (-1 from a failed step on); the state says how far the run got.
+  HIP_TRY(m, hipMemcpyAsync(tokens_out, m->ds + m->L.hist + (size_t)pos0 * 4, (size_t)n * 4,
+                            hipMemcpyDeviceToHost, m->stream));
+  HIP_TRY(m, hipMemcpyAsync(m->h_state, m->ds + m->L.state, sizeof(DecodeState),
+                            hipMemcpyDeviceToHost, m->stream));
+  if (logits)
+    HIP_TRY(m, hipMemcpyAsync(logits, m->ds + m->L.logits, (size_t)m->cfg.vocab * 4,
+                              hipMemcpyDeviceToHost, m->stream));
+  HIP_TRY(m, hipStreamSynchronize(m->stream));
+  m->pos = m->h_state->pos;
+  const int32_t steps = m->pos - pos0;
+  if (m->h_state->bad) {
+    m->have_token = false;
+    *n_done = steps - 1;
+    for (int32_t i = steps - 1; i < n; ++i) tokens_out[i] = -1;
+    return fail(m, WICI_E_NUMERIC, "non-finite logits at position %d (step %d of %d)", m->pos - 1,
+                steps, n);
+  }
+  if (steps != n) {
+    m->failed = true;
+    return fail(m, WICI_E_HIP, "device ran %d of %d steps", steps, n);
+  }
+  *n_done = n;
+  m->have_token = true;
+  return WICI_OK;
 }
 
 wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,

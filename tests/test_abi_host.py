@@ -89,6 +89,13 @@ def test_state_machine_before_memory_is_bound():
         assert lib.wici_prefill(h, toks, 3, ctypes.byref(out), None) == binding.WICI_E_STATE
         assert lib.wici_decode_step(h, -1, ctypes.byref(out), None) == binding.WICI_E_STATE
         assert lib.wici_decode_step(h, 1000, ctypes.byref(out), None) == binding.WICI_E_ARG
+        gen = (ctypes.c_int32 * 4)()
+        done = ctypes.c_int32(7)
+        assert lib.wici_decode_n(h, -1, 4, gen, None, None) == binding.WICI_E_ARG
+        assert lib.wici_decode_n(h, -1, 0, gen, ctypes.byref(done), None) == binding.WICI_E_ARG
+        assert done.value == 0
+        assert lib.wici_decode_n(h, 1000, 4, gen, ctypes.byref(done), None) == binding.WICI_E_ARG
+        assert lib.wici_decode_n(h, -1, 4, gen, ctypes.byref(done), None) == binding.WICI_E_STATE
         assert lib.wici_reset_kv(h) == binding.WICI_E_STATE
         buf = (ctypes.c_uint16 * 64)()
         assert lib.wici_read_kv(h, 0, 0, 1, buf, buf) == binding.WICI_E_STATE

@@ -48,6 +48,11 @@ def test_full_size_greedy_run_matches_oracle(cuda_ok, name, mode):
     try:
         m.load_weights(w)
         ids, logs = m.generate(prompt, cfg.decode_steps, want_logits=True)
+        # the same request with the decode steps run device-resident in one call
+        m.reset_kv()
+        first, _ = m.prefill(prompt)
+        toks, _ = m.decode_n(cfg.decode_steps)
+        ids_n = [first] + [int(t) for t in toks]
     finally:
         m.close()
     t1 = time.time()
@@ -68,3 +73,4 @@ def test_full_size_greedy_run_matches_oracle(cuda_ok, name, mode):
         f.write(json.dumps(rec) + "\n")
     assert rep.max_rel_err <= 2e-2, rec
     assert rep.strict_ids, rec
+    assert ids_n == [int(i) for i in ids], "wici_decode_n differs from wici_decode_step"
