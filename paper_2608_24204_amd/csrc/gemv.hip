@@ -12,13 +12,21 @@
 //    the chip streams a contiguous band of rows;
 //  - a row group is ROWS complete rows (two for a gate/up pair of the SwiGLU
 //    epilogue) read with 64 lanes x 16 B = 1 KiB coalesced loads, in batches of
-//    U sweeps of 512 elements; the next batch is issued before the current one
-//    is consumed (double buffering), so loads never stop at row boundaries;
-//  - the first batch is issued before the prologue, which stages x * gain in
-//    LDS; an RMS-normalised input gets its 1/rms factor applied to the finished
-//    row sums (W (x g r) = r W (x g)), so one barrier publishes the vector;
-//  - row sums are reduced with DPP row operations; after the prologue no
-//    wavefront ever waits for another.
+//    U sweeps of 512 elements; the next batch is in flight while the current
+//    one is consumed (double buffering), so loads never stop at row boundaries.
+//
+// Vector-memory completions are counted in issue order, and the compiler can
+// only wait for "all but the last n" when n is the same on every path.  So
+// every load is unconditional (addresses clamped into the matrix; lanes past
+// the row end are loaded but never used), finished rows go to LDS rather than
+// to global memory, and the loop is peeled so that its two issues are
+// unconditional: consuming a batch then waits for that batch alone, with the
+// next one still in flight.  The prologue issues all loads of x (and the norm
+// gain, and the residual values this wavefront will update) first, then the
+// first weight batch, and waits for x alone; an RMS-normalised input gets its
+// 1/rms factor applied to the finished row sums (W (x g r) = r W (x g)), so
+// one barrier publishes the staged vector.  Row sums are reduced with DPP row
+// operations; each wavefront writes its rows at the end.
 #include "common.h"
 #include "kernels.h"
 
@@ -63,14 +71,21 @@ struct Batch {
   Vec8<WT> w[ROWS][U];
 };
 
-template <typename WT, int EPI, bool NORM, int ROWS, int U>
+// Rounds of x staging: each round is 8 float4 per thread (8192 floats per
+// workgroup), all issued before the first weight batch.
+constexpr int kMaxGemvK = 32768;
+
+template <typename WT, int EPI, bool NORM, int ROWS, int U, int XR>
 __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, int K,
                                               const float* __restrict__ x,
                                               const float* __restrict__ gain, float eps,
                                               float* __restrict__ y,
-                                              ArgmaxPart* __restrict__ part) {
+                                              ArgmaxPart* __restrict__ part, int max_out) {
   static_assert(EPI != GEMV_SWIGLU || ROWS % 2 == 0, "SwiGLU needs whole gate/up pairs");
-  extern __shared__ float xs[];  // K floats
+  constexpr int OPG = EPI == GEMV_SWIGLU ? ROWS / 2 : ROWS;  // outputs per row group
+  extern __shared__ float smem[];
+  float* xs = smem;          // K floats: x * gain
+  float* ys = smem + K;      // [4 wavefronts][max_out] finished outputs
   __shared__ float red[4];
   __shared__ float am_v[4];
   __shared__ int am_i[4];
@@ -81,50 +96,58 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
   const int wid = blockIdx.x * 4 + wave, nw = gridDim.x * 4;
   const int my_groups = wid < ngroups ? (ngroups - 1 - wid) / nw + 1 : 0;
   const int nbatch = my_groups * nsb;
+  const int nout = my_groups * OPG;
+  const int nf4 = K >> 2;
+  // global row (or SwiGLU output) index of this wavefront's output j
+  auto out_row = [&](int j) {
+    const int gi = j / OPG, o = j - gi * OPG;
+    return EPI == GEMV_SWIGLU ? (wid + gi * nw) * OPG + o : (wid + gi * nw) * ROWS + o;
+  };
+  const int n_rows_out = EPI == GEMV_SWIGLU ? N / 2 : N;
 
-  // issue batch b into buf (rows past N and lanes past K read nothing)
+  // issue batch b into buf: always ROWS x U loads (row and column clamped)
   auto issue = [&](Batch<WT, ROWS, U>& buf, int b) {
     const int gi = b / nsb, s0 = (b - gi * nsb) * U;
     const int r0 = (wid + gi * nw) * ROWS;
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
-      const WT* wr = W + (size_t)min(r0 + r, N - 1) * K + lane * 8;
+      const WT* wr = W + (size_t)min(r0 + r, N - 1) * K;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int k = (s0 + u) * 512 + lane * 8;
-        if (r0 + r < N && k < K) ld(buf.w[r][u], wr + (s0 + u) * 512);
-        else zero(buf.w[r][u]);
-      }
+      for (int u = 0; u < U; ++u) ld(buf.w[r][u], wr + min((s0 + u) * 512 + lane * 8, K - 8));
     }
   };
 
+  // ---- prologue: x, gain and residual loads, then the first weight batch ----------
+  float4 xv[XR][8], xg[NORM ? XR : 1][8];
+#pragma unroll
+  for (int r = 0; r < XR; ++r)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int f = min(r * 2048 + u * 256 + tid, nf4 - 1);
+      xv[r][u] = reinterpret_cast<const float4*>(x)[f];
+      if (NORM) xg[NORM ? r : 0][u] = reinterpret_cast<const float4*>(gain)[f];
+    }
+  float yres = 0.f;
+  if (EPI == GEMV_RESID) yres = y[min(out_row(lane), n_rows_out - 1)];
   Batch<WT, ROWS, U> b0, b1;
-  if (nbatch > 0) issue(b0, 0);
+  issue(b0, 0);
 
-  // ---- stage x * gain in LDS, sum of squares for the norm ---------------------------
   float ss = 0.f;
-  {
-    constexpr int SU = 4;
-    for (int k0 = tid * 4; k0 < K; k0 += 1024 * SU) {
-      float4 v[SU];
 #pragma unroll
-      for (int u = 0; u < SU; ++u)
-        if (k0 + u * 1024 < K) v[u] = *reinterpret_cast<const float4*>(x + k0 + u * 1024);
+  for (int r = 0; r < XR; ++r)
 #pragma unroll
-      for (int u = 0; u < SU; ++u) {
-        const int k = k0 + u * 1024;
-        if (k < K) {
-          float4 t = v[u];
-          if (NORM) {
-            ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
-            const float4 g = *reinterpret_cast<const float4*>(gain + k);
-            t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
-          }
-          *reinterpret_cast<float4*>(xs + k) = t;
+    for (int u = 0; u < 8; ++u) {
+      const int f = r * 2048 + u * 256 + tid;
+      if (f < nf4) {
+        float4 t = xv[r][u];
+        if (NORM) {
+          const float4 g = xg[NORM ? r : 0][u];
+          ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
+          t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
         }
+        reinterpret_cast<float4*>(xs)[f] = t;
       }
     }
-  }
   if (NORM) {
     ss = wave_sum(ss);
     if (lane == 0) red[wave] = ss;
@@ -136,9 +159,7 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
   float acc[ROWS];
 #pragma unroll
   for (int r = 0; r < ROWS; ++r) acc[r] = 0.f;
-  float best_v = -INFINITY;
-  int best_i = 0x7fffffff;
-  bool bad = false;
+  float* yw = ys + wave * max_out;
 
   auto consume = [&](const Batch<WT, ROWS, U>& buf, int b) {
     const int gi = b / nsb, sb = b - gi * nsb, s0 = sb * U;
@@ -152,25 +173,15 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
       }
     }
     if (sb == nsb - 1) {  // row group complete
-      const int r0 = (wid + gi * nw) * ROWS;
 #pragma unroll
       for (int r = 0; r < ROWS; ++r) acc[r] = wave_sum(acc[r]) * rnorm;
-      if (EPI == GEMV_SWIGLU) {
+      if (lane == 0) {
+        if (EPI == GEMV_SWIGLU) {
 #pragma unroll
-        for (int r = 0; r < ROWS; r += 2)
-          if (lane == r && r0 + r + 1 < N) y[(r0 + r) >> 1] = silu(acc[r]) * acc[r + 1];
-      } else {
+          for (int r = 0; r < ROWS; r += 2) yw[gi * OPG + r / 2] = silu(acc[r]) * acc[r + 1];
+        } else {
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r) {
-          if (lane == r && r0 + r < N) {
-            if (EPI == GEMV_RESID) y[r0 + r] += acc[r];
-            else y[r0 + r] = acc[r];
-          }
-          if (EPI == GEMV_ARGMAX && r0 + r < N) {
-            // NaN never compares better; a non-finite logit is flagged separately
-            if (am_better(acc[r], r0 + r, best_v, best_i)) { best_v = acc[r]; best_i = r0 + r; }
-            bad |= !isfinite(acc[r]);
-          }
+          for (int r = 0; r < ROWS; ++r) yw[gi * OPG + r] = acc[r];
         }
       }
 #pragma unroll
@@ -178,29 +189,60 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
     }
   };
 
-  // double-buffered stream of batches: issue b+1, consume b
-  for (int b = 0; b < nbatch; b += 2) {
-    if (b + 1 < nbatch) issue(b1, b + 1);
+  // ---- double-buffered stream of batches (steady state: unconditional issues) -----
+  int b = 0;
+  for (; b + 2 < nbatch; b += 2) {
+    issue(b1, b + 1);
     consume(b0, b);
-    if (b + 1 < nbatch) {
-      if (b + 2 < nbatch) issue(b0, b + 2);
-      consume(b1, b + 1);
-    }
+    issue(b0, b + 2);
+    consume(b1, b + 1);
+  }
+  if (b + 1 < nbatch) {
+    issue(b1, b + 1);
+    consume(b0, b);
+    consume(b1, b + 1);
+  } else if (b < nbatch) {
+    consume(b0, b);
   }
 
+  // ---- outputs of this wavefront (its own LDS slots: no barrier needed) -----------
+  float best_v = -INFINITY;
+  int best_i = 0x7fffffff;
+  bool bad = false;
+  for (int j = lane; j < nout; j += 64) {
+    const int row = out_row(j);
+    const float v = yw[j];
+    if (row < n_rows_out) {
+      if (EPI == GEMV_RESID) y[row] = (j < 64 ? yres : y[row]) + v;
+      else y[row] = v;
+      if (EPI == GEMV_ARGMAX) {
+        // NaN never compares better; a non-finite logit is flagged separately
+        if (am_better(v, row, best_v, best_i)) { best_v = v; best_i = row; }
+        bad |= !isfinite(v);
+      }
+    }
+  }
   if (EPI == GEMV_ARGMAX) {
-    // a non-finite logit marks the partial with index -1
+    // (value, lowest index) over the workgroup; a non-finite logit marks the
+    // partial with index -1
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      const float ov = __shfl_xor(best_v, m);
+      const int oi = __shfl_xor(best_i, m);
+      if (am_better(ov, oi, best_v, best_i)) { best_v = ov; best_i = oi; }
+      bad |= __shfl_xor((int)bad, m) != 0;
+    }
     if (lane == 0) { am_v[wave] = best_v; am_i[wave] = bad ? -1 : best_i; }
     __syncthreads();
     if (tid == 0) {
       float bv = am_v[0]; int bi = am_i[0];
-      bool b = bi < 0;
+      bool bb = bi < 0;
       for (int w = 1; w < 4; ++w) {
-        b |= am_i[w] < 0;
+        bb |= am_i[w] < 0;
         if (am_better(am_v[w], am_i[w], bv, bi)) { bv = am_v[w]; bi = am_i[w]; }
       }
       part[blockIdx.x].v = bv;
-      part[blockIdx.x].i = b ? -1 : bi;
+      part[blockIdx.x].i = bb ? -1 : bi;
     }
   }
 }
@@ -209,18 +251,31 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
 template <typename WT, int EPI, int ROWS, int U>
 hipError_t launch_gemv_cfg(const WT* W, int N, int K, const float* x, const float* gain,
                            float eps, float* y, ArgmaxPart* part, int grid, hipStream_t st) {
-  const size_t lds = (size_t)K * sizeof(float);
-#define WICI_GEMV_NORM(NR)                                                                   \
+  if (K < 8 || K % 8 || K > kMaxGemvK || N < 1 || grid < 1) return hipErrorInvalidValue;
+  constexpr int OPG = EPI == GEMV_SWIGLU ? ROWS / 2 : ROWS;
+  const int ngroups = (N + ROWS - 1) / ROWS, nw = grid * 4;
+  const int max_out = (ngroups + nw - 1) / nw * OPG;
+  const size_t lds = ((size_t)K + 4 * (size_t)max_out) * sizeof(float);
+  const int xr = K <= 8192 ? 1 : K <= 16384 ? 2 : 4;
+#define WICI_GEMV_GO(NR, XR)                                                                 \
   do {                                                                                       \
+    auto fn = &k_gemv<WT, EPI, NR, ROWS, U, XR>;                                             \
     if (lds > 65536)                                                                         \
-      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemv<WT, EPI, NR, ROWS, U>), \
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),                           \
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);       \
-    hipLaunchKernelGGL((k_gemv<WT, EPI, NR, ROWS, U>), dim3(grid), dim3(256), lds, st, W, N, K, \
-                       x, gain, eps, y, part);                                               \
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(256), lds, st, W, N, K, x, gain, eps, y, part,   \
+                       max_out);                                                             \
   } while (0)
-  if (gain) WICI_GEMV_NORM(true);
-  else WICI_GEMV_NORM(false);
-#undef WICI_GEMV_NORM
+#define WICI_GEMV_XR(NR)                   \
+  do {                                     \
+    if (xr == 1) WICI_GEMV_GO(NR, 1);      \
+    else if (xr == 2) WICI_GEMV_GO(NR, 2); \
+    else WICI_GEMV_GO(NR, 4);              \
+  } while (0)
+  if (gain) WICI_GEMV_XR(true);
+  else WICI_GEMV_XR(false);
+#undef WICI_GEMV_XR
+#undef WICI_GEMV_GO
   return hipGetLastError();
 }
 

@@ -53,6 +53,9 @@ bool config_ok(const wici_config* c, std::string* why) {
     return bad("query heads per KV head must be 1, 2, 4, 5 or 8");
   if (c->max_seq > 16384) return bad("max_seq above 16384");
   if (c->n_heads > 128) return bad("at most 128 query heads");
+  // the decode GEMV stages its whole input vector in LDS
+  if (c->d_model > 32768 || c->ffn_dim > 32768 || c->n_heads * c->head_dim > 32768)
+    return bad("d_model, ffn_dim and n_heads*head_dim must be at most 32768");
   if (c->vocab < 1) return bad("vocab must be >= 1");
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return bad("rms_eps must be > 0");
   if (!(c->rope_base > 1.0) || !std::isfinite(c->rope_base)) return bad("rope_base must be > 1");
