@@ -25,19 +25,21 @@ __device__ __forceinline__ size_t kv_off(const KvLayout& kv, int pos, int which,
 // ------------------------------------------------------------------- decode
 // Grid (nsplit, Hkv): block (s, g) owns positions [64 s, 64 s + 64) of KV head g;
 // blocks past the current context exit at once, so one captured launch serves
-// every position.  The block's page-table entries are read before the position
-// is known and all of its cached keys and values are requested before the query
-// is rotated.  Each block writes its unnormalised output and (max, sum)
-// statistics; a second kernel merges the splits.  (Merging in the last block of
-// each head would need device-scope fences, whose L2 write-back and invalidate
-// on every block cost more than the extra launch.)
+// every position.  The queries arrive rotated and pre-scaled, and the new
+// position's key and value are already in the cache (both done by the QKV
+// projection's epilogue), so a block's loads depend only on its page-table
+// entries and on the position, which arrive together: every slot of the chunk
+// is then requested at once (slots past the context are loaded and ignored).
+// Each block writes
+// its unnormalised output and (max, sum) statistics; a second kernel merges the
+// splits.  (Merging in the last block of each head would need device-scope
+// fences, whose L2 write-back and invalidate on every block cost more than the
+// extra launch.)
 constexpr int kChunk = 64;       // positions per decode split
 constexpr int kMaxSplits = 256;  // splits the merge kernel holds in LDS
 
 template <int HD, typename KT, int G>
-__global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ qkv, int Hq,
-                                                     const float* __restrict__ cos_t,
-                                                     const float* __restrict__ sin_t,
+__global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q_in,
                                                      KvLayout kv,
                                                      const DecodeState* __restrict__ st,
                                                      float* __restrict__ part_o,
@@ -46,10 +48,8 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
   constexpr int PPW = 64 / LPP;     // positions per wave per pass
   constexpr int PPB = 4 * PPW;      // positions per block per pass
   constexpr int NP = kChunk / PPB;  // passes over the chunk
-  constexpr int HALF = HD / 2;
   __shared__ float qs[G][HD];
   __shared__ float sc[G][kChunk];
-  __shared__ float knew[HD], vnew[HD];
   __shared__ float accs[4][G][HD];
   __shared__ float mls[G][2];
 
@@ -59,64 +59,38 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int pg = lane / LPP, sub = lane % LPP;
   const int start = split * kChunk;
-  // page of each of this lane's positions (independent of the current position)
+  const KT* base = static_cast<const KT*>(kv.base);
+  const size_t head_stride = (size_t)kv.page * HD;
+  // page of each of this lane's positions (clamped into the table)
   int phys[NP];
 #pragma unroll
   for (int i = 0; i < NP; ++i) {
     const int j = start + i * PPB + wave * PPW + pg;
     phys[i] = kv.table[min(j, kv.max_pos - 1) / kv.page];
   }
+  // queries of the group (independent of the position)
+  float qv[(G * HD + 255) / 256];
+#pragma unroll
+  for (int k = 0; k < (G * HD + 255) / 256; ++k)
+    qv[k] = q_in[(size_t)g * G * HD + min(tid + k * 256, G * HD - 1)];
+  // the position (a scalar load, back as soon as the table entries): blocks past
+  // the context stop before requesting anything more
   const int pos = st->pos, n = pos + 1;
   if (start >= n) return;
   const int end = min(n, start + kChunk);
-  const KT* base = static_cast<const KT*>(kv.base);
-  const size_t head_stride = (size_t)kv.page * HD;
-  auto addr = [&](int p, int j, int which) {
-    return base + (((size_t)p * 2 + which) * Hkv + g) * head_stride + (size_t)(j % kv.page) * HD;
-  };
-
-  // ---- request every cached key/value of the chunk --------------------------------
+  // every slot of the chunk: keys and values
   float kr[NP][8], vr[NP][8];
 #pragma unroll
   for (int i = 0; i < NP; ++i) {
     const int j = start + i * PPB + wave * PPW + pg;
-    if (j < end && j != pos) {
-      load8(addr(phys[i], j, 0) + sub * 8, kr[i]);
-      load8(addr(phys[i], j, 1) + sub * 8, vr[i]);
-    }
+    const KT* pk = base + (((size_t)phys[i] * 2 + 0) * Hkv + g) * head_stride +
+                   (size_t)(j % kv.page) * HD + sub * 8;
+    load8(pk, kr[i]);
+    load8(pk + (size_t)Hkv * head_stride, vr[i]);
   }
-
-  // ---- rotated, pre-scaled queries; the new position's key/value ------------------
-  const float scale = 1.0f / sqrtf((float)HD);
-  const float* cr = cos_t + (size_t)pos * HALF;
-  const float* sr = sin_t + (size_t)pos * HALF;
-  for (int i = tid; i < G * HALF; i += 256) {
-    const int h = i / HALF, j = i % HALF;
-    const float* z = qkv + (size_t)(g * G + h) * HD;
-    const float a = z[j], b = z[j + HALF], c = cr[j], s = sr[j];
-    qs[h][j] = (a * c - b * s) * scale;
-    qs[h][j + HALF] = (a * s + b * c) * scale;
-  }
-  if (end == n) {  // this split holds the new position: rotate, round, append
-    const float* kz = qkv + (size_t)Hq * HD + (size_t)g * HD;
-    const float* vz = kz + (size_t)Hkv * HD;
-    const int pp = kv.table[pos / kv.page];
-    KT* kd = const_cast<KT*>(addr(pp, pos, 0));
-    KT* vd = const_cast<KT*>(addr(pp, pos, 1));
-    for (int j = tid; j < HALF; j += 256) {
-      const float a = kz[j], b = kz[j + HALF], c = cr[j], s = sr[j];
-      const float ra = Elem<KT>::round(a * c - b * s), rb = Elem<KT>::round(a * s + b * c);
-      knew[j] = ra;
-      knew[j + HALF] = rb;
-      Elem<KT>::store(kd + j, ra);
-      Elem<KT>::store(kd + j + HALF, rb);
-    }
-    for (int e = tid; e < HD; e += 256) {
-      const float v = Elem<KT>::round(vz[e]);
-      vnew[e] = v;
-      Elem<KT>::store(vd + e, v);
-    }
-  }
+#pragma unroll
+  for (int k = 0; k < (G * HD + 255) / 256; ++k)
+    if (tid + k * 256 < G * HD) (&qs[0][0])[tid + k * 256] = qv[k];
   __syncthreads();
 
   // ---- scores ------------------------------------------------------------------------
@@ -131,10 +105,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
 #pragma unroll
   for (int i = 0; i < NP; ++i) {
     const int j = start + i * PPB + wave * PPW + pg;
-    if (j == pos) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) { kr[i][e] = knew[sub * 8 + e]; vr[i][e] = vnew[sub * 8 + e]; }
-    } else if (j >= end) {
+    if (j >= end) {  // past the context: whatever the slot holds is not used
 #pragma unroll
       for (int e = 0; e < 8; ++e) { kr[i][e] = 0.f; vr[i][e] = 0.f; }
     }
@@ -266,27 +237,26 @@ __global__ __launch_bounds__(HD) void k_attn_merge(const float* __restrict__ par
 }
 
 template <int HD, typename KT, int G>
-static hipError_t attn_decode_t(const float* qkv, int Hq, const float* cos_t, const float* sin_t,
-                                KvLayout kv, const DecodeState* st, int nsplit, float* part_o,
-                                float* part_ml, float* out, hipStream_t s) {
-  hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv), dim3(256), 0, s, qkv,
-                     Hq, cos_t, sin_t, kv, st, part_o, part_ml);
+static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const DecodeState* st,
+                                int nsplit, float* part_o, float* part_ml, float* out,
+                                hipStream_t s) {
+  hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv), dim3(256), 0, s, q, kv,
+                     st, part_o, part_ml);
   hipLaunchKernelGGL((k_attn_merge<HD>), dim3(Hq), dim3(HD), 0, s, part_o, part_ml, nsplit, st,
                      out);
   return hipGetLastError();
 }
 
 template <int HD, typename KT>
-static hipError_t attn_decode_g(int G, const float* qkv, int Hq, const float* cos_t,
-                                const float* sin_t, KvLayout kv, const DecodeState* st,
-                                int nsplit, float* part_o, float* part_ml, float* out,
-                                hipStream_t s) {
+static hipError_t attn_decode_g(int G, const float* q, int Hq, KvLayout kv,
+                                const DecodeState* st, int nsplit, float* part_o,
+                                float* part_ml, float* out, hipStream_t s) {
   switch (G) {
-    case 1: return attn_decode_t<HD, KT, 1>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
-    case 2: return attn_decode_t<HD, KT, 2>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
-    case 4: return attn_decode_t<HD, KT, 4>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
-    case 5: return attn_decode_t<HD, KT, 5>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
-    case 8: return attn_decode_t<HD, KT, 8>(qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    case 1: return attn_decode_t<HD, KT, 1>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    case 2: return attn_decode_t<HD, KT, 2>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    case 4: return attn_decode_t<HD, KT, 4>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    case 5: return attn_decode_t<HD, KT, 5>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    case 8: return attn_decode_t<HD, KT, 8>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -294,19 +264,20 @@ static hipError_t attn_decode_g(int G, const float* qkv, int Hq, const float* co
 int attn_decode_splits(int max_seq) { return (max_seq + kChunk - 1) / kChunk; }
 bool attn_group_supported(int G) { return G == 1 || G == 2 || G == 4 || G == 5 || G == 8; }
 
-hipError_t launch_attn_decode(bool kv_bf16, const float* qkv, int Hq, const float* cos_t,
-                              const float* sin_t, KvLayout kv, const void* state, int nsplit,
-                              float* part_o, float* part_ml, float* out, hipStream_t s) {
-  if (nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos) return hipErrorInvalidValue;
+hipError_t launch_attn_decode(bool kv_bf16, const float* q, int Hq, KvLayout kv,
+                              const void* state, int nsplit, float* part_o, float* part_ml,
+                              float* out, hipStream_t s) {
+  if (nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos || kv.n_kv < 1 || Hq % kv.n_kv)
+    return hipErrorInvalidValue;
   const DecodeState* st = static_cast<const DecodeState*>(state);
   const int G = Hq / kv.n_kv;
   if (kv.hd == 128) {
-    if (kv_bf16) return attn_decode_g<128, bf16_t>(G, qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
-    return attn_decode_g<128, float>(G, qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    if (kv_bf16) return attn_decode_g<128, bf16_t>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    return attn_decode_g<128, float>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
   }
   if (kv.hd == 64) {
-    if (kv_bf16) return attn_decode_g<64, bf16_t>(G, qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
-    return attn_decode_g<64, float>(G, qkv, Hq, cos_t, sin_t, kv, st, nsplit, part_o, part_ml, out, s);
+    if (kv_bf16) return attn_decode_g<64, bf16_t>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    return attn_decode_g<64, float>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
   }
   return hipErrorInvalidValue;
 }

@@ -80,8 +80,10 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
                                               const float* __restrict__ x,
                                               const float* __restrict__ gain, float eps,
                                               float* __restrict__ y,
-                                              ArgmaxPart* __restrict__ part, int max_out) {
+                                              ArgmaxPart* __restrict__ part, int max_out,
+                                              QkvRope rope) {
   static_assert(EPI != GEMV_SWIGLU || ROWS % 2 == 0, "SwiGLU needs whole gate/up pairs");
+  static_assert(EPI != GEMV_QKV || ROWS == 2, "QKV row groups are RoPE pairs");
   constexpr int OPG = EPI == GEMV_SWIGLU ? ROWS / 2 : ROWS;  // outputs per row group
   extern __shared__ float smem[];
   float* xs = smem;          // K floats: x * gain
@@ -105,13 +107,24 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
   };
   const int n_rows_out = EPI == GEMV_SWIGLU ? N / 2 : N;
 
+  // matrix row of member r of row group g: consecutive rows, or for QKV the RoPE
+  // pair (j, j + hd/2) of head g / (hd/2)
+  const int half = rope.kv.hd >> 1;
+  auto grow = [&](int g, int r) {
+    if (EPI == GEMV_QKV) {
+      const int hh = g / half;
+      return hh * 2 * half + (g - hh * half) + r * half;
+    }
+    return g * ROWS + r;
+  };
+
   // issue batch b into buf: always ROWS x U loads (row and column clamped)
   auto issue = [&](Batch<WT, ROWS, U>& buf, int b) {
     const int gi = b / nsb, s0 = (b - gi * nsb) * U;
-    const int r0 = (wid + gi * nw) * ROWS;
+    const int g = wid + gi * nw;
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
-      const WT* wr = W + (size_t)min(r0 + r, N - 1) * K;
+      const WT* wr = W + (size_t)min(grow(g, r), N - 1) * K;
 #pragma unroll
       for (int u = 0; u < U; ++u) ld(buf.w[r][u], wr + min((s0 + u) * 512 + lane * 8, K - 8));
     }
@@ -131,6 +144,17 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
   if (EPI == GEMV_RESID) yres = y[min(out_row(lane), n_rows_out - 1)];
   Batch<WT, ROWS, U> b0, b1;
   issue(b0, 0);
+  // QKV: the position, its KV page, and this lane's rotation (group `lane`)
+  int pos = 0, phys = 0;
+  float rc = 0.f, rs = 0.f;
+  if (EPI == GEMV_QKV) {
+    pos = static_cast<const DecodeState*>(rope.state)->pos;
+    phys = rope.kv.table[pos / rope.kv.page];
+    const int g = min(wid + lane * nw, ngroups - 1);
+    const int j = g - (g / half) * half;
+    rc = rope.cos_t[(size_t)pos * half + j];
+    rs = rope.sin_t[(size_t)pos * half + j];
+  }
 
   float ss = 0.f;
 #pragma unroll
@@ -206,6 +230,36 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
   }
 
   // ---- outputs of this wavefront (its own LDS slots: no barrier needed) -----------
+  if (EPI == GEMV_QKV) {
+    const KvLayout& kv = rope.kv;
+    const int slot = pos % kv.page;
+    for (int gi = lane; gi < my_groups; gi += 64) {
+      const int g = wid + gi * nw, hh = g / half, j = g - hh * half;
+      const float a = yw[2 * gi], b = yw[2 * gi + 1];
+      const float c = gi < 64 ? rc : rope.cos_t[(size_t)pos * half + j];
+      const float sn = gi < 64 ? rs : rope.sin_t[(size_t)pos * half + j];
+      if (hh < rope.n_q) {
+        y[(size_t)hh * 2 * half + j] = (a * c - b * sn) * rope.q_scale;
+        y[(size_t)hh * 2 * half + j + half] = (a * sn + b * c) * rope.q_scale;
+      } else {
+        const int which = hh < rope.n_q + kv.n_kv ? 0 : 1;  // key or value head
+        const int h = hh - rope.n_q - which * kv.n_kv;
+        const float va = which ? a : a * c - b * sn, vb = which ? b : a * sn + b * c;
+        const size_t off =
+            ((((size_t)phys * 2 + which) * kv.n_kv + h) * kv.page + slot) * kv.hd + j;
+        if (rope.kv_bf16) {
+          bf16_t* d = static_cast<bf16_t*>(kv.base) + off;
+          d[0] = f32_to_bf16(va);
+          d[half] = f32_to_bf16(vb);
+        } else {
+          float* d = static_cast<float*>(kv.base) + off;
+          d[0] = va;
+          d[half] = vb;
+        }
+      }
+    }
+    return;
+  }
   float best_v = -INFINITY;
   int best_i = 0x7fffffff;
   bool bad = false;
@@ -250,8 +304,16 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
 // Launch shape: ROWS rows per group, U sweeps per batch, `grid` workgroups.
 template <typename WT, int EPI, int ROWS, int U>
 hipError_t launch_gemv_cfg(const WT* W, int N, int K, const float* x, const float* gain,
-                           float eps, float* y, ArgmaxPart* part, int grid, hipStream_t st) {
+                           float eps, float* y, ArgmaxPart* part, int grid, hipStream_t st,
+                           const QkvRope* rope = nullptr) {
   if (K < 8 || K % 8 || K > kMaxGemvK || N < 1 || grid < 1) return hipErrorInvalidValue;
+  QkvRope rp{};
+  rp.kv.hd = 2;  // unused outside GEMV_QKV (keeps the pair arithmetic defined)
+  if (EPI == GEMV_QKV) {
+    if (!rope || rope->kv.hd < 2 || rope->kv.hd % 2 || N != (rope->n_q + 2 * rope->kv.n_kv) * rope->kv.hd)
+      return hipErrorInvalidValue;
+    rp = *rope;
+  }
   constexpr int OPG = EPI == GEMV_SWIGLU ? ROWS / 2 : ROWS;
   const int ngroups = (N + ROWS - 1) / ROWS, nw = grid * 4;
   const int max_out = (ngroups + nw - 1) / nw * OPG;
@@ -264,7 +326,7 @@ hipError_t launch_gemv_cfg(const WT* W, int N, int K, const float* x, const floa
       (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),                           \
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);       \
     hipLaunchKernelGGL(fn, dim3(grid), dim3(256), lds, st, W, N, K, x, gain, eps, y, part,   \
-                       max_out);                                                             \
+                       max_out, rp);                                                         \
   } while (0)
 #define WICI_GEMV_XR(NR)                   \
   do {                                     \
@@ -297,33 +359,40 @@ int gemv_argmax_blocks(int N) { return gemv_shape(N, 0).grid; }
 template <typename WT, int EPI>
 static hipError_t gemv_dispatch(const GemvShape& s, const WT* W, int N, int K, const float* x,
                                 const float* gain, float eps, float* y, ArgmaxPart* part,
-                                hipStream_t st) {
+                                hipStream_t st, const QkvRope* rope) {
   // the same bytes per batch for both weight types
   if (sizeof(WT) == 2)
-    return launch_gemv_cfg<WT, EPI, 2, 4>(W, N, K, x, gain, eps, y, part, s.grid, st);
-  return launch_gemv_cfg<WT, EPI, 2, 2>(W, N, K, x, gain, eps, y, part, s.grid, st);
+    return launch_gemv_cfg<WT, EPI, 2, 4>(W, N, K, x, gain, eps, y, part, s.grid, st, rope);
+  return launch_gemv_cfg<WT, EPI, 2, 2>(W, N, K, x, gain, eps, y, part, s.grid, st, rope);
 }
 
 template <typename WT>
 static hipError_t gemv_t(int epi, const WT* W, int N, int K, const float* x, const float* gain,
-                         float eps, float* y, ArgmaxPart* part, hipStream_t st) {
+                         float eps, float* y, ArgmaxPart* part, hipStream_t st,
+                         const QkvRope* rope) {
   const GemvShape s = gemv_shape(N, K);
+#define WICI_GEMV_EPI(E) \
+  case E: return gemv_dispatch<WT, E>(s, W, N, K, x, gain, eps, y, part, st, rope)
   switch (epi) {
-    case GEMV_STORE: return gemv_dispatch<WT, GEMV_STORE>(s, W, N, K, x, gain, eps, y, part, st);
-    case GEMV_RESID: return gemv_dispatch<WT, GEMV_RESID>(s, W, N, K, x, gain, eps, y, part, st);
-    case GEMV_SWIGLU: return gemv_dispatch<WT, GEMV_SWIGLU>(s, W, N, K, x, gain, eps, y, part, st);
-    case GEMV_ARGMAX: return gemv_dispatch<WT, GEMV_ARGMAX>(s, W, N, K, x, gain, eps, y, part, st);
+    WICI_GEMV_EPI(GEMV_STORE);
+    WICI_GEMV_EPI(GEMV_RESID);
+    WICI_GEMV_EPI(GEMV_SWIGLU);
+    WICI_GEMV_EPI(GEMV_ARGMAX);
+    WICI_GEMV_EPI(GEMV_QKV);
     default: return hipErrorInvalidValue;
   }
+#undef WICI_GEMV_EPI
 }
 
 hipError_t launch_gemv(bool w_bf16, int epi, const void* W, int N, int K, const float* x,
                        const float* norm_gain, float eps, float* y, ArgmaxPart* part,
-                       int* nblocks, hipStream_t st) {
+                       int* nblocks, hipStream_t st, const QkvRope* rope) {
   if (nblocks) *nblocks = gemv_shape(N, K).grid;
   if (w_bf16)
-    return gemv_t<bf16_t>(epi, static_cast<const bf16_t*>(W), N, K, x, norm_gain, eps, y, part, st);
-  return gemv_t<float>(epi, static_cast<const float*>(W), N, K, x, norm_gain, eps, y, part, st);
+    return gemv_t<bf16_t>(epi, static_cast<const bf16_t*>(W), N, K, x, norm_gain, eps, y, part,
+                          st, rope);
+  return gemv_t<float>(epi, static_cast<const float*>(W), N, K, x, norm_gain, eps, y, part, st,
+                       rope);
 }
 
 }  // namespace wici

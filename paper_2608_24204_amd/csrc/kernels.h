@@ -6,18 +6,47 @@
 
 namespace wici {
 
-enum GemvEpi { GEMV_STORE = 0, GEMV_RESID = 1, GEMV_SWIGLU = 2, GEMV_ARGMAX = 3 };
+enum GemvEpi { GEMV_STORE = 0, GEMV_RESID = 1, GEMV_SWIGLU = 2, GEMV_ARGMAX = 3, GEMV_QKV = 4 };
 
 struct ArgmaxPart { float v; int32_t i; };
+
+struct KvLayout {
+  void* base;            // this layer's pool
+  const int32_t* table;  // logical page -> physical page
+  int page;              // positions per page
+  int n_kv;              // KV heads
+  int hd;                // head dim
+  int max_pos;           // capacity (positions); the table covers ceil(max_pos / page) pages
+  // element offset of (phys page, kv 0/1, head h, slot s, dim d):
+  //   ((phys * 2 + kv) * n_kv + h) * page * hd + s * hd + d
+};
+
+// The decode QKV projection's epilogue (GEMV_QKV): RoPE at the current position
+// and the KV-cache append.  W is [(n_q + 2 n_kv) * hd, K] (query heads, then key
+// heads, then value heads); the GEMV walks it in RoPE pairs (rows j and j + hd/2
+// of a head), so each finished pair is rotated in registers:
+//   query heads: y[h*hd + j], y[h*hd + j + hd/2] = rotated values * q_scale;
+//   key heads:   rotated values, rounded to the cache type, stored at the position;
+//   value heads: values rounded to the cache type, stored at the position.
+struct QkvRope {
+  const float* cos_t;  // [max_pos][hd/2]
+  const float* sin_t;
+  const void* state;   // DecodeState: the position being appended
+  KvLayout kv;         // this layer's cache (kv.hd = head dim, kv.n_kv = KV heads)
+  int kv_bf16;         // cache element type: 1 bf16, 0 fp32
+  int n_q;             // query heads
+  float q_scale;       // 1/sqrt(hd)
+};
 
 // y = W x for W [N, K] row-major (bf16 bits or fp32), x fp32 [K].
 // norm_gain != nullptr: x is first RMS-normalised (eps) and scaled by the gain.
 // STORE: y[n] = acc.  RESID: y[n] += acc.  SWIGLU: rows (2i, 2i+1) hold
 // (gate_i, up_i) and y[i] = silu(gate_i) * up_i.  ARGMAX: y[n] = acc and one
 // ArgmaxPart per block into `part` (grid size returned through *nblocks).
+// QKV: as described for QkvRope (`rope` required, N = (n_q + 2 n_kv) * hd).
 hipError_t launch_gemv(bool w_bf16, int epi, const void* W, int N, int K, const float* x,
                        const float* norm_gain, float eps, float* y, ArgmaxPart* part,
-                       int* nblocks, hipStream_t st);
+                       int* nblocks, hipStream_t st, const QkvRope* rope = nullptr);
 int gemv_argmax_blocks(int N);
 
 // Final argmax over `n` partials -> st->token; st->pos += advance (or = set_pos
@@ -42,16 +71,6 @@ hipError_t launch_init_block_table(int32_t* table, int n_pages, hipStream_t st);
 hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int T, int d,
                                const ActBuf& y, hipStream_t st);
 
-struct KvLayout {
-  void* base;            // this layer's pool
-  const int32_t* table;  // logical page -> physical page
-  int page;              // positions per page
-  int n_kv;              // KV heads
-  int hd;                // head dim
-  int max_pos;           // capacity (positions); the table covers ceil(max_pos / page) pages
-  // element offset of (phys page, kv 0/1, head h, slot s, dim d):
-  //   ((phys * 2 + kv) * n_kv + h) * page * hd + s * hd + d
-};
 
 // Prefill: rotate q (in place) and k of T rows at positions p0..p0+T-1 and
 // append k, v to the cache.  qkv rows are [Hq*hd | Hkv*hd | Hkv*hd] fp32.
@@ -64,13 +83,14 @@ hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
                                KvLayout kv, const ActBuf& out, hipStream_t st);
 
-// Decode attention at position state->pos: rotates q and the new k, appends the
-// new k, v, attends over [0, pos] in splits of 64 positions (grid nsplit x Hkv,
-// nsplit = attn_decode_splits(max_seq)) and merges them into out [Hq*hd] fp32.
-hipError_t launch_attn_decode(bool kv_bf16, const float* qkv, int Hq, const float* cos_t,
-                              const float* sin_t, KvLayout kv, const void* state,
-                              int nsplit, float* part_o, float* part_ml, float* out,
-                              hipStream_t st);
+// Decode attention at position state->pos: q = the rotated, pre-scaled queries
+// [Hq*hd] (the QKV GEMV's GEMV_QKV output), keys and values = cache positions
+// [0, pos] (the new position already appended by that GEMV); splits of 64
+// positions (grid nsplit x Hkv, nsplit = attn_decode_splits(max_seq)) merged
+// into out [Hq*hd] fp32.
+hipError_t launch_attn_decode(bool kv_bf16, const float* q, int Hq, KvLayout kv,
+                              const void* state, int nsplit, float* part_o, float* part_ml,
+                              float* out, hipStream_t st);
 int attn_decode_splits(int max_seq);
 bool attn_group_supported(int G);
 

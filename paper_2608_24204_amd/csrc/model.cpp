@@ -258,11 +258,18 @@ hipError_t enqueue_decode(wici_model* m, std::vector<hipEvent_t>* marks = nullpt
   if ((e = mark())) return e;
   WICI_STEP(wici::launch_embed(wb, m->dw + L.embed, d, nullptr, 1, st, x, s));
   for (int l = 0; l < c.n_layers; ++l) {
-    WICI_STEP(wici::launch_gemv(wb, wici::GEMV_STORE, m->dw + m->layer(l, L.l_wqkv), nqkv, d, x,
+    wici::QkvRope rope{};
+    rope.cos_t = m->W<float>(L.rope_cos);
+    rope.sin_t = m->W<float>(L.rope_sin);
+    rope.state = st;
+    rope.kv = m->kv(l);
+    rope.kv_bf16 = kb ? 1 : 0;
+    rope.n_q = c.n_heads;
+    rope.q_scale = 1.0f / std::sqrt((float)c.head_dim);
+    WICI_STEP(wici::launch_gemv(wb, wici::GEMV_QKV, m->dw + m->layer(l, L.l_wqkv), nqkv, d, x,
                                 m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, qkv, nullptr,
-                                nullptr, s));
-    WICI_STEP(wici::launch_attn_decode(kb, qkv, c.n_heads, m->W<float>(L.rope_cos),
-                                       m->W<float>(L.rope_sin), m->kv(l), st, L.nsplit,
+                                nullptr, s, &rope));
+    WICI_STEP(wici::launch_attn_decode(kb, qkv, c.n_heads, m->kv(l), st, L.nsplit,
                                        m->S<float>(L.part_o), m->S<float>(L.part_ml), att, s));
     WICI_STEP(wici::launch_gemv(wb, wici::GEMV_RESID, m->dw + m->layer(l, L.l_wo), d, qd, att,
                                 nullptr, 0.f, x, nullptr, nullptr, s));
