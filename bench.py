@@ -71,8 +71,9 @@ def measured_traffic(cfg):
 
 
 def profile_pass(model, cfg, prompt, n_decode):
-    """Eager decode steps with HIP events around every launch (same positions as a
-    timed request).  Returns mean per-launch ms per kernel class and per-token sums."""
+    """Eager decode steps, each launch timed by start/stop events recorded by its
+    kernels' dispatches (same positions as a timed request).  Returns mean
+    per-launch ms per kernel class and per-token sums."""
     model.reset_kv()
     model.prefill(prompt)
     L = cfg.n_layers
@@ -217,7 +218,7 @@ def main(argv=None):
     }
 
     if not args.no_profile:
-        log("profiling pass (eager launches, HIP events)")
+        log("profiling pass (eager launches timed by dispatch-recorded HIP events)")
         mean, per_tok = profile_pass(model, cfg, prompt, n_decode)
         gu = gateup_bytes(cfg)
         ach = gu / (mean["gateup"] / 1e3)
@@ -225,8 +226,9 @@ def main(argv=None):
                            "bound": "hbm", "achieved": ach / 1e9, "peak": HBM_PEAK / 1e9,
                            "unit": "GB/s", "frac": ach / HBM_PEAK, "traffic": measured_traffic(cfg),
                            "bytes_per_launch": gu, "avg_launch_ms": mean["gateup"],
-                           "method": "HIP events around each launch, eager profiling pass over "
-                                     "one request's decode steps"}
+                           "method": "start/stop HIP events recorded by the kernel's dispatch "
+                                     "(hipExtLaunchKernelGGL) on the model's stream, eager "
+                                     "profiling pass over one request's decode steps"}
         res["decode_kernel_ms_per_token"] = per_tok
         res["decode_kernel_sum_ms"] = float(sum(per_tok.values()))
         res["decode_step_ms"] = 1e3 / decode_tok_s

@@ -187,13 +187,15 @@ wici_status wici_read_kv(wici_model* m, int32_t layer, int32_t begin, int32_t en
                          void* host_k, void* host_v);
 
 /* Diagnostic: one decode step exactly as wici_decode_step (same arguments, checks
- * and state effects) but launched eagerly, with a HIP event recorded on the
- * model's stream around every kernel launch.  Writes the duration in ms of each
- * launch, in launch order, to durations_ms (capacity entries) and their number
- * (3 + 5 * n_layers) to *n_written.  Order: embedding; per layer: QKV GEMV,
- * attention (split pass + merge), O GEMV, gate/up GEMV, down GEMV; then the LM
- * head GEMV and the final argmax.  Errors as wici_decode_step, plus WICI_E_ARG
- * for NULL outputs or a capacity below 3 + 5 * n_layers. */
+ * and state effects) but launched eagerly, each launch timed by HIP events that
+ * its kernels' dispatches record as the first kernel starts and the last one
+ * ends (kernel execution time, without the gaps between launches).  Writes the
+ * duration in ms of each launch, in launch order, to durations_ms (capacity
+ * entries) and their number (3 + 5 * n_layers) to *n_written.  Order: embedding;
+ * per layer: QKV GEMV (with RoPE and the KV append), attention (split pass
+ * start to merge end), O GEMV, gate/up GEMV, down GEMV; then the LM head GEMV
+ * and the final argmax.  Errors as wici_decode_step, plus WICI_E_ARG for NULL
+ * outputs or a capacity below 3 + 5 * n_layers. */
 wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
                                      float* durations_ms, int32_t capacity, int32_t* n_written);
 

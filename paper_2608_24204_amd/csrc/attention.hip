@@ -12,6 +12,7 @@
 // fp32 query and probabilities split into bf16 terms), else fp32 vector code.
 #include "common.h"
 #include "kernels.h"
+#include "launch.h"
 
 namespace wici {
 
@@ -240,10 +241,9 @@ template <int HD, typename KT, int G>
 static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const DecodeState* st,
                                 int nsplit, float* part_o, float* part_ml, float* out,
                                 hipStream_t s) {
-  hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv), dim3(256), 0, s, q, kv,
-                     st, part_o, part_ml);
-  hipLaunchKernelGGL((k_attn_merge<HD>), dim3(Hq), dim3(HD), 0, s, part_o, part_ml, nsplit, st,
-                     out);
+  launch_k(k_attn_decode<HD, KT, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv, st,
+           part_o, part_ml);
+  launch_k(k_attn_merge<HD>, dim3(Hq), dim3(HD), 0, s, kLast, part_o, part_ml, nsplit, st, out);
   return hipGetLastError();
 }
 

@@ -29,6 +29,7 @@
 // operations; each wavefront writes its rows at the end.
 #include "common.h"
 #include "kernels.h"
+#include "launch.h"
 
 namespace wici {
 
@@ -325,8 +326,8 @@ hipError_t launch_gemv_cfg(const WT* W, int N, int K, const float* x, const floa
     if (lds > 65536)                                                                         \
       (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),                           \
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);       \
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(256), lds, st, W, N, K, x, gain, eps, y, part,   \
-                       max_out, rp);                                                         \
+    launch_k(fn, dim3(grid), dim3(256), lds, st, kOnly, W, N, K, x, gain, eps, y, part,      \
+             max_out, rp);                                                                   \
   } while (0)
 #define WICI_GEMV_XR(NR)                   \
   do {                                     \

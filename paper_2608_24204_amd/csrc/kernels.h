@@ -10,6 +10,13 @@ enum GemvEpi { GEMV_STORE = 0, GEMV_RESID = 1, GEMV_SWIGLU = 2, GEMV_ARGMAX = 3,
 
 struct ArgmaxPart { float v; int32_t i; };
 
+// Timing of the decode launchers (used by the profiling entry point): while set
+// on the calling thread, a launcher's first kernel records `start` when it begins
+// and its last kernel records `stop` when it ends.
+struct LaunchTimer { hipEvent_t start; hipEvent_t stop; };
+void set_launch_timer(const LaunchTimer* t);
+const LaunchTimer* launch_timer();
+
 struct KvLayout {
   void* base;            // this layer's pool
   const int32_t* table;  // logical page -> physical page

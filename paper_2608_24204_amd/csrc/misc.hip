@@ -3,8 +3,15 @@
 // device-side step state.
 #include "common.h"
 #include "kernels.h"
+#include "launch.h"
 
 namespace wici {
+
+namespace {
+thread_local const LaunchTimer* g_launch_timer = nullptr;
+}
+void set_launch_timer(const LaunchTimer* t) { g_launch_timer = t; }
+const LaunchTimer* launch_timer() { return g_launch_timer; }
 
 // ---- embedding ------------------------------------------------------------------
 template <typename WT>
@@ -31,10 +38,10 @@ hipError_t launch_embed(bool w_bf16, const void* E, int d, const int32_t* tokens
                         const void* state, float* x, hipStream_t st) {
   const DecodeState* s = static_cast<const DecodeState*>(state);
   if (w_bf16)
-    hipLaunchKernelGGL(k_embed<bf16_t>, dim3(T), dim3(256), 0, st,
+    launch_k(k_embed<bf16_t>, dim3(T), dim3(256), 0, st, kOnly,
                        static_cast<const bf16_t*>(E), d, tokens, s, x);
   else
-    hipLaunchKernelGGL(k_embed<float>, dim3(T), dim3(256), 0, st,
+    launch_k(k_embed<float>, dim3(T), dim3(256), 0, st, kOnly,
                        static_cast<const float*>(E), d, tokens, s, x);
   return hipGetLastError();
 }
@@ -198,7 +205,7 @@ __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restr
 
 hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int32_t* hist,
                                int advance, int set_pos, hipStream_t st) {
-  hipLaunchKernelGGL(k_argmax_final, dim3(1), dim3(1024), 0, st, part, n,
+  launch_k(k_argmax_final, dim3(1), dim3(1024), 0, st, kOnly, part, n,
                      static_cast<DecodeState*>(state), hist, advance, set_pos);
   return hipGetLastError();
 }

@@ -227,9 +227,10 @@ void build_specs(wici_model* m) {
 bool usable(const wici_model* m) { return m && !m->failed; }
 
 // Enqueue one decode step (position and input token read from device state).
-// With `marks`, an event is recorded before the first launch and after every
-// launcher call (the profiling entry point uses this; graph capture never does).
-hipError_t enqueue_decode(wici_model* m, std::vector<hipEvent_t>* marks = nullptr) {
+// With `timers`, every launcher call is timed: a start/stop event pair recorded
+// by the dispatches of its first and last kernel (the profiling entry point uses
+// this; graph capture never does).
+hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers = nullptr) {
   const wici_config& c = m->cfg;
   const Layout& L = m->L;
   const bool wb = c.weight_dtype == WICI_BF16, kb = c.kv_dtype == WICI_BF16;
@@ -242,20 +243,26 @@ hipError_t enqueue_decode(wici_model* m, std::vector<hipEvent_t>* marks = nullpt
   void* st = m->ds + L.state;
   hipStream_t s = m->stream;
   hipError_t e;
-  auto mark = [&]() -> hipError_t {
-    if (!marks) return hipSuccess;
-    hipEvent_t ev;
-    hipError_t r = hipEventCreate(&ev);
-    if (r != hipSuccess) return r;
-    marks->push_back(ev);
-    return hipEventRecord(ev, s);
+  wici::LaunchTimer cur{};
+  auto arm = [&]() -> hipError_t {
+    if (!timers) return hipSuccess;
+    hipError_t r = hipEventCreate(&cur.start);
+    if (r == hipSuccess) r = hipEventCreate(&cur.stop);
+    if (r == hipSuccess) wici::set_launch_timer(&cur);
+    return r;
   };
-#define WICI_STEP(call) \
-  do {                  \
-    if ((e = (call))) return e; \
-    if ((e = mark())) return e; \
+  auto disarm = [&]() {
+    if (!timers) return;
+    wici::set_launch_timer(nullptr);
+    timers->push_back(cur);
+  };
+#define WICI_STEP(call)         \
+  do {                          \
+    if ((e = arm())) return e;  \
+    e = (call);                 \
+    disarm();                   \
+    if (e) return e;            \
   } while (0)
-  if ((e = mark())) return e;
   WICI_STEP(wici::launch_embed(wb, m->dw + L.embed, d, nullptr, 1, st, x, s));
   for (int l = 0; l < c.n_layers; ++l) {
     wici::QkvRope rope{};
@@ -628,18 +635,24 @@ wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* n
   if (m->pos + 1 > m->cfg.max_seq)
     return fail(m, WICI_E_CAPACITY, "position %d reached max_seq", m->pos);
   if (token_in >= 0) HIP_TRY(m, wici::launch_set_token(m->ds + m->L.state, token_in, m->stream));
-  std::vector<hipEvent_t> ev;
-  const hipError_t e = enqueue_decode(m, &ev);
+  std::vector<wici::LaunchTimer> tv;
+  const hipError_t e = enqueue_decode(m, &tv);
   const hipError_t e2 = e == hipSuccess ? hipStreamSynchronize(m->stream) : e;
   int n = 0;
+  hipError_t e3 = hipSuccess;
   if (e2 == hipSuccess)
-    for (size_t i = 1; i < ev.size(); ++i) {
+    for (const wici::LaunchTimer& t : tv) {
       float ms = 0.f;
-      if (hipEventElapsedTime(&ms, ev[i - 1], ev[i]) == hipSuccess) durations_ms[n] = ms;
-      ++n;
+      const hipError_t r = hipEventElapsedTime(&ms, t.start, t.stop);
+      if (r != hipSuccess && e3 == hipSuccess) e3 = r;
+      durations_ms[n++] = ms;
     }
-  for (hipEvent_t x : ev) (void)hipEventDestroy(x);
+  for (const wici::LaunchTimer& t : tv) {
+    if (t.start) (void)hipEventDestroy(t.start);
+    if (t.stop) (void)hipEventDestroy(t.stop);
+  }
   HIP_TRY(m, e2);
+  HIP_TRY(m, e3);
   *n_written = n;
   return finish_step(m, next_token, nullptr);
 }
