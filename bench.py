@@ -97,10 +97,11 @@ def cpu_baseline(cfg, w, n_prompt, n_decode):
     the GPU path can be compared with it."""
     from threadpoolctl import threadpool_info
 
-    from oracle import DecoderOracle, greedy
+    from oracle import DecoderOracle, greedy, q8_model_f64
     from paper_2608_24204_amd import inputs
     t0 = time.perf_counter()
-    w64 = inputs.weights_f64(cfg, w)
+    # a block-scaled 8-bit model: the oracle quantises the same source weights itself
+    w64 = q8_model_f64(w) if cfg.weight_dtype == "q8" else inputs.weights_f64(cfg, w)
     conv_s = time.perf_counter() - t0
     prompt = inputs.make_prompt(cfg, n_prompt)
     orc = DecoderOracle(cfg, w64, max_seq=n_prompt + n_decode + 1)
@@ -117,8 +118,9 @@ def cpu_baseline(cfg, w, n_prompt, n_decode):
     out = {"value": n_decode / (t2 - t1), "unit": "tokens/s", "cores": int(threads),
            "kind": "oracle",
            "sample": f"{cfg.name}: prefill of {n_prompt} prompt ids then {n_decode} greedy decode "
-                     f"steps, float64 numpy on the host (weights widened to float64 beforehand, "
-                     f"{conv_s:.1f} s, not timed)",
+                     f"steps, float64 numpy on the host (weights "
+                     f"{'quantised by the oracle and ' if cfg.weight_dtype == 'q8' else ''}"
+                     f"widened to float64 beforehand, {conv_s:.1f} s, not timed)",
            "prefill_tok_s": n_prompt / (t1 - t0), "ttft_ms": (t1 - t0) * 1e3,
            "host_cpus": os.cpu_count()}
     return out, (prompt, ids, logs)

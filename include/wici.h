@@ -49,7 +49,10 @@ typedef enum {
   WICI_E_NUMERIC = -5   /* a logit was NaN or infinite; no token is returned */
 } wici_status;
 
-typedef enum { WICI_F32 = 0, WICI_BF16 = 1 } wici_dtype;
+/* Element types.  WICI_Q8 is a weight storage format only (wici_config's
+ * weight_dtype): block-scaled 8-bit codes, see wici_quantize_q8; its weight
+ * tensors are given as WICI_BF16 or WICI_F32 and quantised at load. */
+typedef enum { WICI_F32 = 0, WICI_BF16 = 1, WICI_Q8 = 2 } wici_dtype;
 
 /* Arithmetic of the prefill projections (decode always multiplies bf16/fp32
  * weights by fp32 activations with fp32 accumulation). */
@@ -198,6 +201,24 @@ wici_status wici_read_kv(wici_model* m, int32_t layer, int32_t begin, int32_t en
  * outputs or a capacity below 3 + 5 * n_layers. */
 wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
                                      float* durations_ms, int32_t capacity, int32_t* n_written);
+
+/* Block-scaled 8-bit quantisation of a row-major matrix [rows, cols] (host
+ * memory; cols a multiple of 32), the storage of WICI_Q8 weights.  The paper's
+ * models are stored at about 8.5 bits per weight (Sec. "Experiment Setup", Tab.
+ * "model_conf"); this format spends exactly that: each row is cut into blocks of
+ * 32 weights along cols, and a block keeps one half-precision scale
+ *   d = fp16(max_i |w_i| / 127)             (float32 division, ties to even)
+ * and 32 codes
+ *   q_i = clamp(rint(w_i / d), -127, 127)   (float32 division, ties to even;
+ *                                            q_i = 0 when d == 0),
+ * so the model computes with w'_i = q_i * d.  Output: codes[rows*cols] holds
+ * q_i + 128 as unsigned bytes, scales[rows*(cols/32)] the half-precision bit
+ * patterns, both row-major.  src_dtype is WICI_F32 or WICI_BF16 (bit patterns).
+ * Host only (no GPU call; multi-threaded for large matrices).  Errors:
+ * WICI_E_ARG for NULL pointers, bad sizes or dtype, a non-finite weight or a
+ * block scale that overflows half precision (outputs then partly written). */
+wici_status wici_quantize_q8(const void* src, int32_t src_dtype, int64_t rows, int64_t cols,
+                             uint8_t* codes, uint16_t* scales);
 
 /* Message of the last failed call on this model ("" if none).  Valid until the
  * next call on the model. */

@@ -80,10 +80,21 @@ def quantize_q8_loops(w) -> tuple[np.ndarray, np.ndarray]:
     return q, d
 
 
-def quantized_weights_f64(tensors: dict, names) -> dict:
-    """float64 dequantised copies of the named float32 matrices (others untouched)."""
-    out = dict(tensors)
-    for n in names:
-        q, d = quantize_q8(tensors[n])
-        out[n] = dequantize_q8(q, d)
-    return out
+def q8_model_f64(weights: dict, threads: int = 16) -> dict:
+    """Oracle weights of a block-scaled 8-bit model from its source tensors (bf16 bit
+    patterns as uint16, or float32): every matrix quantised and dequantised to
+    float64, every vector (norm gains) widened to float64."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    def one(item):
+        name, a = item
+        a = np.asarray(a)
+        f = (a.astype(np.uint32) << 16).view(np.float32) if a.dtype == np.uint16 else \
+            a.astype(np.float32)
+        if f.ndim == 2:
+            q, d = quantize_q8(f)
+            return name, dequantize_q8(q, d)
+        return name, f.astype(np.float64)
+
+    with ThreadPoolExecutor(max(1, threads)) as ex:
+        return dict(ex.map(one, weights.items()))

@@ -21,14 +21,15 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwici.so"
 WICI_OK, WICI_E_ARG, WICI_E_STATE, WICI_E_CAPACITY, WICI_E_HIP, WICI_E_NUMERIC = 0, -1, -2, -3, -4, -5
 STATUS_NAMES = {0: "WICI_OK", -1: "WICI_E_ARG", -2: "WICI_E_STATE", -3: "WICI_E_CAPACITY",
                 -4: "WICI_E_HIP", -5: "WICI_E_NUMERIC"}
-WICI_F32, WICI_BF16 = 0, 1
+WICI_F32, WICI_BF16, WICI_Q8 = 0, 1, 2
 PREFILL_MODES = {"bf16x2": 0, "bf16": 1, "f32": 2, "bf16x3": 3}
 WICI_FLAG_NO_GRAPH = 1
 
 # every entry point include/wici.h declares
 EXPORTED = ["wici_create", "wici_memory_requirements", "wici_bind_memory", "wici_load_weights",
             "wici_prefill", "wici_decode_step", "wici_decode_n", "wici_reset_kv", "wici_position",
-            "wici_read_kv", "wici_profile_decode_step", "wici_last_error", "wici_destroy"]
+            "wici_read_kv", "wici_profile_decode_step", "wici_quantize_q8", "wici_last_error",
+            "wici_destroy"]
 
 
 class WiciConfig(ctypes.Structure):
@@ -83,6 +84,7 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
         "wici_read_kv": ([P, i32, i32, i32, P, P], ctypes.c_int),
         "wici_profile_decode_step": ([P, i32, ctypes.POINTER(i32), P, i32, ctypes.POINTER(i32)],
                                      ctypes.c_int),
+        "wici_quantize_q8": ([P, i32, ctypes.c_int64, ctypes.c_int64, P, P], ctypes.c_int),
         "wici_last_error": ([P], ctypes.c_char_p),
         "wici_destroy": ([P], None),
     }
@@ -105,7 +107,7 @@ def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool =
     c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab = cfg.n_kv_heads, cfg.head_dim, cfg.ffn_dim, cfg.vocab
     c.rms_eps, c.rope_base = cfg.rms_eps, cfg.rope_base
     c.tied_embeddings = int(cfg.tied_embeddings)
-    c.weight_dtype = WICI_BF16 if cfg.weight_dtype == "bf16" else WICI_F32
+    c.weight_dtype = {"bf16": WICI_BF16, "f32": WICI_F32, "q8": WICI_Q8}[cfg.weight_dtype]
     c.kv_dtype = WICI_BF16 if cfg.kv_dtype == "bf16" else WICI_F32
     c.max_seq = cfg.max_seq if max_seq is None else max_seq
     c.prefill_chunk = cfg.prefill_chunk if prefill_chunk is None else prefill_chunk
@@ -113,6 +115,23 @@ def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool =
     c.prefill_mode = PREFILL_MODES[prefill_mode]
     c.flags = 0 if graph else WICI_FLAG_NO_GRAPH
     return c
+
+
+def quantize_q8(w: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """The library's host quantiser (wici_quantize_q8) on a float32 or bf16-bits
+    (uint16) matrix [rows, cols]: returns (codes uint8 = q + 128, scales as float16)."""
+    lib = load_library()
+    w = np.ascontiguousarray(w)
+    dt = WICI_BF16 if w.dtype == np.uint16 else WICI_F32
+    if dt == WICI_F32:
+        w = np.ascontiguousarray(w, dtype=np.float32)
+    rows, cols = w.shape
+    codes = np.empty((rows, cols), np.uint8)
+    scales = np.empty((rows, cols // 32), np.uint16)
+    st = lib.wici_quantize_q8(w.ctypes.data, dt, rows, cols, codes.ctypes.data, scales.ctypes.data)
+    if st != WICI_OK:
+        raise WiciError(st, "wici_quantize_q8")
+    return codes, scales.view(np.float16)
 
 
 def memory_requirements(c: WiciConfig) -> tuple[int, int, int]:

@@ -28,7 +28,8 @@ class ModelConfig:
     rms_eps: float = 1e-5    # reading: the only value stated for any workload, used for all
     rope_base: float = 10000.0
     tied_embeddings: bool = False
-    weight_dtype: str = "bf16"   # "bf16" or "f32"
+    weight_dtype: str = "bf16"   # "bf16", "f32", or "q8" (bf16 source weights stored as
+                                 # block-scaled 8-bit codes: 34 bytes per 32 weights)
     kv_dtype: str = "bf16"       # KV cache storage type
     prompt_len: int = 32
     decode_steps: int = 16
@@ -54,8 +55,8 @@ class ModelConfig:
         return self.prompt_len + self.decode_steps
 
     @property
-    def wbytes(self) -> int:
-        return 2 if self.weight_dtype == "bf16" else 4
+    def wbytes(self) -> float:
+        return {"bf16": 2, "f32": 4, "q8": 34 / 32}[self.weight_dtype]
 
     @property
     def kvbytes(self) -> int:
@@ -80,7 +81,7 @@ class ModelConfig:
         once, the KV cache read once per KV head, and one new KV position written."""
         w = (self.n_layers * self.layer_matrix_params() + self.vocab * self.d_model) * self.wbytes
         kv_read = n_ctx * self.n_layers * 2 * self.kv_dim * self.kvbytes
-        return w + kv_read
+        return int(round(w)) + kv_read
 
     def prefill_flops(self, n_prompt: int | None = None) -> int:
         """Algorithmic flops of a prefill: projections of every prompt row, causal
@@ -118,7 +119,15 @@ QWEN_32B = ModelConfig(
     rope_base=1000000.0,      # reading: not stated; the shape family's value
     prompt_len=2048, decode_steps=128)
 
-CONFIGS = {c.name: c for c in (TINY, LLAMA_1B, LLAMA_8B, LLAMA_8B_LONG, QWEN_32B)}
+# The same models with their matrices stored block-scaled in 8 bits (the paper's
+# applications run quantised GGUF models of about 8.5 bits per weight); same keys,
+# so the same bf16 source weights.
+LLAMA_1B_Q8 = LLAMA_1B.with_(name="1b_q8", weight_dtype="q8")
+LLAMA_8B_Q8 = LLAMA_8B.with_(name="8b_q8", weight_dtype="q8")
+QWEN_32B_Q8 = QWEN_32B.with_(name="32b_q8", weight_dtype="q8")
+
+CONFIGS = {c.name: c for c in (TINY, LLAMA_1B, LLAMA_8B, LLAMA_8B_LONG, QWEN_32B,
+                               LLAMA_1B_Q8, LLAMA_8B_Q8, QWEN_32B_Q8)}
 
 
 def reduced(cfg: ModelConfig, n_layers: int, key_offset: int = 100, **kw) -> ModelConfig:

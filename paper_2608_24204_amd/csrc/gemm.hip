@@ -41,13 +41,22 @@ __device__ __forceinline__ void epi_out(float* C, int ldc, const ActBuf& H, int 
 constexpr int kBK = 32;   // K per step (one v_mfma_f32_16x16x32_bf16 depth)
 constexpr int kLDK = 40;  // padded LDS row (bf16 elements)
 
-template <int NT, int WM, int WN, int EPI>
+// Q8 weights: a step of 32 along K is one quantisation block, so the codes go
+// through the matrix cores exactly (an integer in [-127, 127] is a bf16 value),
+// the NT products of a step are summed in a fresh accumulator, and that sum is
+// multiplied by the column's block scale and added: one scale multiply per
+// step and output, the products staying exact.
+template <int NT, int WM, int WN, int EPI, bool Q8>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
-    const bf16_t* __restrict__ A, size_t a_plane, int lda, const bf16_t* __restrict__ W, int M,
-    int N, int K, float* __restrict__ C, int ldc, ActBuf H, int ldh) {
+    const bf16_t* __restrict__ A, size_t a_plane, int lda, const void* __restrict__ Wv, int M,
+    int N, int K, float* __restrict__ C, int ldc, ActBuf H, int ldh,
+    const unsigned short* __restrict__ S) {
   constexpr int BM = 64 * WM, BN = 64 * WN, NTH = 64 * WM * WN;
   constexpr int A_CHUNKS = NT * BM * (kBK / 8);  // 16-byte chunks per step
-  constexpr int W_CHUNKS = BN * (kBK / 8);
+  constexpr int W_CHUNKS = BN * (Q8 ? kBK / 16 : kBK / 8);
+  constexpr int WCPR = Q8 ? 2 : 4;               // weight chunks per row and step
+  const bf16_t* W = static_cast<const bf16_t*>(Wv);
+  const uint8_t* Wq = static_cast<const uint8_t*>(Wv);
   constexpr int A_PER = (A_CHUNKS + NTH - 1) / NTH;
   constexpr int W_PER = (W_CHUNKS + NTH - 1) / NTH;
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
@@ -80,11 +89,31 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
     for (int i = 0; i < W_PER; ++i) {
       const int c = tid + i * NTH;
       if (c < W_CHUNKS) {
-        const int row = c / 4, part = c % 4, n = n0 + row;
-        rw[i] = n < N ? *reinterpret_cast<const uint4*>(W + (size_t)n * K + k0 + part * 8)
-                      : make_uint4(0, 0, 0, 0);
+        const int row = c / WCPR, part = c % WCPR, n = n0 + row;
+        if (Q8)
+          rw[i] = n < N ? *reinterpret_cast<const uint4*>(Wq + (size_t)n * K + k0 + part * 16)
+                        : make_uint4(0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u);
+        else
+          rw[i] = n < N ? *reinterpret_cast<const uint4*>(W + (size_t)n * K + k0 + part * 8)
+                        : make_uint4(0, 0, 0, 0);
       }
     }
+  };
+  // Q8: the block scales of this lane's four output columns for step kt, loaded
+  // one step ahead together with that step's tiles
+  const int fr = lane & 15, fk = (lane >> 4) * 8;
+  unsigned short scq[4];
+  float scn[4];
+  auto sload = [&](int kt) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = min(n0 + wn * 64 + j * 16 + fr, N - 1);
+      scq[j] = S[(size_t)n * (K / 32) + kt];
+    }
+  };
+  auto sfix = [&]() {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) scn[j] = (float)__builtin_bit_cast(_Float16, scq[j]);
   };
   auto sstore = [&](int s) {
 #pragma unroll
@@ -99,8 +128,24 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
     for (int i = 0; i < W_PER; ++i) {
       const int c = tid + i * NTH;
       if (c < W_CHUNKS) {
-        const int row = c / 4, part = c % 4;
-        *reinterpret_cast<uint4*>(Bs + ((size_t)s * BN + row) * kLDK + part * 8) = rw[i];
+        const int row = c / WCPR, part = c % WCPR;
+        if (Q8) {
+          // 16 codes -> 16 bf16 values (code - 128, exact)
+          unsigned o[8];
+          const unsigned wv[4] = {rw[i].x, rw[i].y, rw[i].z, rw[i].w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const unsigned w = wv[e / 2], sh = 16 * (e & 1);
+            const float lo = (float)((w >> sh) & 0xffu) - 128.f;
+            const float hi = (float)((w >> (sh + 8)) & 0xffu) - 128.f;
+            o[e] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xffff0000u);
+          }
+          uint4* dst = reinterpret_cast<uint4*>(Bs + ((size_t)s * BN + row) * kLDK + part * 16);
+          dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+          dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+        } else {
+          *reinterpret_cast<uint4*>(Bs + ((size_t)s * BN + row) * kLDK + part * 8) = rw[i];
+        }
       }
     }
   };
@@ -111,32 +156,60 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int fr = lane & 15, fk = (lane >> 4) * 8;
   const int KT = K / kBK;
+  if (Q8) sload(0);
   gload(0);
   sstore(0);
+  if (Q8) sfix();
   __syncthreads();
   for (int kt = 0; kt < KT; ++kt) {
     const int s = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * kBK);
+    if (kt + 1 < KT) {
+      if (Q8) sload(kt + 1);
+      gload((kt + 1) * kBK);
+    }
     bf16x8_t bfr[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + ((size_t)s * BN + wn * 64 + j * 16 + fr) * kLDK + fk);
+    if constexpr (Q8) {
 #pragma unroll
-    for (int p = 0; p < NT; ++p) {
-      bf16x8_t af[4];
+      for (int i = 0; i < 4; ++i) {
+        floatx4_t part[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(
-            As + (((size_t)s * NT + p) * BM + wm * 64 + i * 16 + fr) * kLDK + fk);
+        for (int j = 0; j < 4; ++j) part[j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+        for (int p = 0; p < NT; ++p) {
+          const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(
+              As + (((size_t)s * NT + p) * BM + wm * 64 + i * 16 + fr) * kLDK + fk);
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            part[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr[j], part[j], 0, 0, 0);
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[i][j][r] += part[j][r] * scn[j];
+      }
+    } else {
+#pragma unroll
+      for (int p = 0; p < NT; ++p) {
+        bf16x8_t af[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          af[i] = *reinterpret_cast<const bf16x8_t*>(
+              As + (((size_t)s * NT + p) * BM + wm * 64 + i * 16 + fr) * kLDK + fk);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
     }
-    if (kt + 1 < KT) sstore(s ^ 1);
+    if (kt + 1 < KT) {
+      sstore(s ^ 1);
+      if (Q8) sfix();
+    }
     __syncthreads();
   }
 
@@ -160,7 +233,7 @@ template <typename WT, int EPI>
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, int lda,
                                                   const WT* __restrict__ W, int M, int N, int K,
                                                   float* __restrict__ C, int ldc, ActBuf H,
-                                                  int ldh) {
+                                                  int ldh, const unsigned short* __restrict__ S) {
   constexpr int BM = 64, BN = 64, BK = 16;
   __shared__ float As[BK][BM + 4];
   __shared__ float Ws[BK][BN + 4];
@@ -174,8 +247,14 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, i
                       : make_float4(0, 0, 0, 0);
     float w[4];
     if (wn < N) {
+      if constexpr (sizeof(WT) == 1) {  // Q8: (code - 128) * block scale
+        const float d = (float)__builtin_bit_cast(_Float16, S[(size_t)wn * (K / 32) + (k0 + lk) / 32]);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = Elem<WT>::load(W + (size_t)wn * K + k0 + lk + e);
+        for (int e = 0; e < 4; ++e) w[e] = ((float)W[(size_t)wn * K + k0 + lk + e] - 128.f) * d;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = Elem<WT>::load(W + (size_t)wn * K + k0 + lk + e);
+      }
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e) w[e] = 0.f;
@@ -206,19 +285,23 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, i
 }
 
 // ------------------------------------------------------------------- launchers
-template <int NT, int WM, int WN, int EPI>
-static hipError_t gemm_mfma_launch(const ActBuf& A, int lda, const bf16_t* W, int M, int N, int K,
+template <int NT, int WM, int WN, int EPI, bool Q8>
+static hipError_t gemm_mfma_launch(const ActBuf& A, int lda, const void* W, int M, int N, int K,
                                    float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
   constexpr int BM = 64 * WM, BN = 64 * WN;
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   const int grid = (tiles + 7) / 8 * 8;
   const size_t lds = (size_t)2 * (NT * BM + BN) * kLDK * sizeof(bf16_t);
-  auto fn = &k_gemm_mfma<NT, WM, WN, EPI>;
+  const unsigned short* S =
+      Q8 ? reinterpret_cast<const unsigned short*>(static_cast<const char*>(W) +
+                                                   q8_scale_offset(N, K))
+         : nullptr;
+  auto fn = &k_gemm_mfma<NT, WM, WN, EPI, Q8>;
   if (lds > 65536)
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   hipLaunchKernelGGL(fn, dim3(grid), dim3(64 * WM * WN), lds, st, A.planes, A.plane_stride, lda,
-                     W, M, N, K, C, ldc, H, ldh);
+                     W, M, N, K, C, ldc, H, ldh, S);
   return hipGetLastError();
 }
 
@@ -226,19 +309,13 @@ static hipError_t gemm_mfma_launch(const ActBuf& A, int lda, const bf16_t* W, in
 // shapes of 1B-32B models at 1-2K rows, it beats 256 x 128 blocks by 14-35%: the
 // smaller block keeps two workgroups resident per CU, which hides the global-load
 // latency of the next K slice better than the halved weight re-reads save.
-template <int NT, int EPI>
-static hipError_t gemm_mfma_nt(const ActBuf& A, int lda, const bf16_t* W, int M, int N, int K,
-                               float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
-  return gemm_mfma_launch<NT, 2, 2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
-}
-
-template <int EPI>
-static hipError_t gemm_mfma(const ActBuf& A, int lda, const bf16_t* W, int M, int N, int K,
+template <int EPI, bool Q8>
+static hipError_t gemm_mfma(const ActBuf& A, int lda, const void* W, int M, int N, int K,
                             float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
   switch (A.nt) {
-    case 1: return gemm_mfma_nt<1, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
-    case 2: return gemm_mfma_nt<2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
-    case 3: return gemm_mfma_nt<3, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+    case 1: return gemm_mfma_launch<1, 2, 2, EPI, Q8>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+    case 2: return gemm_mfma_launch<2, 2, 2, EPI, Q8>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+    case 3: return gemm_mfma_launch<3, 2, 2, EPI, Q8>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -247,33 +324,39 @@ template <typename WT, int EPI>
 static hipError_t gemm_f32(const ActBuf& A, int lda, const WT* W, int M, int N, int K, float* C,
                            int ldc, const ActBuf& H, int ldh, hipStream_t st) {
   dim3 grid((N + 63) / 64, (M + 63) / 64);
+  const unsigned short* S =
+      sizeof(WT) == 1 ? reinterpret_cast<const unsigned short*>(
+                            reinterpret_cast<const char*>(W) + q8_scale_offset(N, K))
+                      : nullptr;
   hipLaunchKernelGGL((k_gemm_f32<WT, EPI>), grid, dim3(256), 0, st, A.f32, lda, W, M, N, K, C,
-                     ldc, H, ldh);
+                     ldc, H, ldh, S);
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(bool w_bf16, int epi, const ActBuf& A, int lda, const void* W, int M, int N,
+hipError_t launch_gemm(int wt, int epi, const ActBuf& A, int lda, const void* W, int M, int N,
                        int K, float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
   if (K % kBK) return hipErrorInvalidValue;
+#define WICI_EPI(CALL)                                      \
+  switch (epi) {                                            \
+    case GEMV_STORE: return CALL(GEMV_STORE);               \
+    case GEMV_RESID: return CALL(GEMV_RESID);               \
+    case GEMV_SWIGLU: return CALL(GEMV_SWIGLU);             \
+    default: return hipErrorInvalidValue;                   \
+  }
   if (A.nt == 0) {
-#define WICI_F32(WT)                                                                            \
-  switch (epi) {                                                                                \
-    case GEMV_STORE: return gemm_f32<WT, GEMV_STORE>(A, lda, static_cast<const WT*>(W), M, N, K, C, ldc, H, ldh, st); \
-    case GEMV_RESID: return gemm_f32<WT, GEMV_RESID>(A, lda, static_cast<const WT*>(W), M, N, K, C, ldc, H, ldh, st); \
-    case GEMV_SWIGLU: return gemm_f32<WT, GEMV_SWIGLU>(A, lda, static_cast<const WT*>(W), M, N, K, C, ldc, H, ldh, st); \
-    default: return hipErrorInvalidValue;                                                       \
-  }
-    if (w_bf16) { WICI_F32(bf16_t) } else { WICI_F32(float) }
+#define WICI_F32(E) gemm_f32<WT_, E>(A, lda, static_cast<const WT_*>(W), M, N, K, C, ldc, H, ldh, st)
+    if (wt == W_BF16) { using WT_ = bf16_t; WICI_EPI(WICI_F32) }
+    if (wt == W_F32) { using WT_ = float; WICI_EPI(WICI_F32) }
+    if (wt == W_Q8) { using WT_ = uint8_t; WICI_EPI(WICI_F32) }
 #undef WICI_F32
+    return hipErrorInvalidValue;
   }
-  if (!w_bf16) return hipErrorInvalidValue;
-  const bf16_t* Wb = static_cast<const bf16_t*>(W);
-  switch (epi) {
-    case GEMV_STORE: return gemm_mfma<GEMV_STORE>(A, lda, Wb, M, N, K, C, ldc, H, ldh, st);
-    case GEMV_RESID: return gemm_mfma<GEMV_RESID>(A, lda, Wb, M, N, K, C, ldc, H, ldh, st);
-    case GEMV_SWIGLU: return gemm_mfma<GEMV_SWIGLU>(A, lda, Wb, M, N, K, C, ldc, H, ldh, st);
-    default: return hipErrorInvalidValue;
-  }
+#define WICI_MF(E) gemm_mfma<E, Q8_>(A, lda, W, M, N, K, C, ldc, H, ldh, st)
+  if (wt == W_BF16) { constexpr bool Q8_ = false; WICI_EPI(WICI_MF) }
+  if (wt == W_Q8) { constexpr bool Q8_ = true; WICI_EPI(WICI_MF) }
+#undef WICI_MF
+#undef WICI_EPI
+  return hipErrorInvalidValue;
 }
 
 }  // namespace wici

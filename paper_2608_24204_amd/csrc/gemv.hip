@@ -34,9 +34,13 @@
 namespace wici {
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-template <typename WT> struct Vec8;   // 8 weights
+// The weights one lane takes per sweep: 8 bf16, 8 fp32 (two loads) or 16 Q8 codes.
+template <typename WT> struct Vec8;
 template <> struct Vec8<bf16_t> { u32x4 a; };
 template <> struct Vec8<float> { u32x4 a, b; };
+template <> struct Vec8<uint8_t> { u32x4 a; };
+template <typename WT> struct LaneElems { static constexpr int n = 8; };
+template <> struct LaneElems<uint8_t> { static constexpr int n = 16; };
 
 // Weights are read exactly once per step: non-temporal loads keep them from
 // displacing the small vectors that are reused from the caches.
@@ -46,6 +50,9 @@ __device__ __forceinline__ void ld(Vec8<bf16_t>& v, const bf16_t* p) {
 __device__ __forceinline__ void ld(Vec8<float>& v, const float* p) {
   v.a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
   v.b = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p) + 1);
+}
+__device__ __forceinline__ void ld(Vec8<uint8_t>& v, const uint8_t* p) {
+  v.a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 __device__ __forceinline__ void zero(Vec8<bf16_t>& v) { v.a = u32x4{0, 0, 0, 0}; }
 __device__ __forceinline__ void zero(Vec8<float>& v) { v.a = u32x4{0, 0, 0, 0}; v.b = v.a; }
@@ -66,11 +73,30 @@ __device__ __forceinline__ float dot8(const Vec8<float>& v, const float* x) {
          __uint_as_float(v.b.z) * xb.z + __uint_as_float(v.b.w) * xb.w;
 }
 
-// Batch b of a wavefront = (row group, first sweep); nsb batches per group.
+// 16 codes (q + 128 in bytes) times 16 x values, as sum(c x); the caller
+// subtracts 128 sum(x) (precomputed per 16-element chunk) and applies the scale.
+__device__ __forceinline__ float dot16(const Vec8<uint8_t>& v, const float* x) {
+  float s = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float4 xv = *reinterpret_cast<const float4*>(x + 4 * w);
+    const unsigned c = v.a[w];
+    s += (float)(c & 0xffu) * xv.x + (float)((c >> 8) & 0xffu) * xv.y +
+         (float)((c >> 16) & 0xffu) * xv.z + (float)(c >> 24) * xv.w;
+  }
+  return s;
+}
+
+// Batch b of a wavefront = (row group, first sweep); nsb batches per group.  Q8
+// batches also carry each lane's block scale per row and sweep.
 template <typename WT, int ROWS, int U>
 struct Batch {
   Vec8<WT> w[ROWS][U];
+  float sc[ROWS][U];
 };
+__device__ __forceinline__ float half_to_f32(unsigned short h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
 
 // Rounds of x staging: each round is 8 float4 per thread (8192 floats per
 // workgroup), all issued before the first weight batch.
@@ -82,18 +108,22 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
                                               const float* __restrict__ gain, float eps,
                                               float* __restrict__ y,
                                               ArgmaxPart* __restrict__ part, int max_out,
-                                              QkvRope rope) {
+                                              QkvRope rope,
+                                              const unsigned short* __restrict__ S) {
   static_assert(EPI != GEMV_SWIGLU || ROWS % 2 == 0, "SwiGLU needs whole gate/up pairs");
   static_assert(EPI != GEMV_QKV || ROWS == 2, "QKV row groups are RoPE pairs");
   constexpr int OPG = EPI == GEMV_SWIGLU ? ROWS / 2 : ROWS;  // outputs per row group
+  constexpr bool Q8 = sizeof(WT) == 1;
+  constexpr int EPL = LaneElems<WT>::n, SW = 64 * EPL;      // elements per lane / sweep
   extern __shared__ float smem[];
-  float* xs = smem;          // K floats: x * gain
-  float* ys = smem + K;      // [4 wavefronts][max_out] finished outputs
+  float* xs = smem;                          // K floats: x * gain
+  float* xsum = smem + K;                    // Q8: sum of each 16 elements of xs
+  float* ys = smem + K + (Q8 ? K / 16 : 0);  // [4 wavefronts][max_out] finished outputs
   __shared__ float red[4];
   __shared__ float am_v[4];
   __shared__ int am_i[4];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int nsweep = (K + 511) >> 9;          // 512-element sweeps per row
+  const int nsweep = (K + SW - 1) / SW;       // sweeps per row
   const int nsb = (nsweep + U - 1) / U;       // batches per row group
   const int ngroups = (N + ROWS - 1) / ROWS;
   const int wid = blockIdx.x * 4 + wave, nw = gridDim.x * 4;
@@ -127,7 +157,12 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
     for (int r = 0; r < ROWS; ++r) {
       const WT* wr = W + (size_t)min(grow(g, r), N - 1) * K;
 #pragma unroll
-      for (int u = 0; u < U; ++u) ld(buf.w[r][u], wr + min((s0 + u) * 512 + lane * 8, K - 8));
+      for (int u = 0; u < U; ++u) {
+        const int k = min((s0 + u) * SW + lane * EPL, K - EPL);
+        ld(buf.w[r][u], wr + k);
+        if (Q8)
+          buf.sc[r][u] = half_to_f32(S[(size_t)min(grow(g, r), N - 1) * (K / 32) + k / 32]);
+      }
     }
   };
 
@@ -178,6 +213,18 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
     if (lane == 0) red[wave] = ss;
   }
   __syncthreads();
+  if (Q8) {  // block sums of the staged vector for the code offset
+    for (int c = tid; c < K / 16; c += 256) {
+      float t = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float4 v = reinterpret_cast<const float4*>(xs)[c * 4 + w];
+        t += (v.x + v.y) + (v.z + v.w);
+      }
+      xsum[c] = t;
+    }
+    __syncthreads();
+  }
   const float rnorm = NORM ? 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)K + eps)
                            : 1.0f;
 
@@ -190,11 +237,17 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
     const int gi = b / nsb, sb = b - gi * nsb, s0 = sb * U;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int k = (s0 + u) * 512 + lane * 8;
+      const int k = (s0 + u) * SW + lane * EPL;
       if (k < K) {
         const float* xk = xs + k;
+        if constexpr (Q8) {
+          const float off = 128.f * xsum[k / 16];
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r) acc[r] += dot8(buf.w[r][u], xk);
+          for (int r = 0; r < ROWS; ++r) acc[r] += buf.sc[r][u] * (dot16(buf.w[r][u], xk) - off);
+        } else {
+#pragma unroll
+          for (int r = 0; r < ROWS; ++r) acc[r] += dot8(buf.w[r][u], xk);
+        }
       }
     }
     if (sb == nsb - 1) {  // row group complete
@@ -318,7 +371,13 @@ hipError_t launch_gemv_cfg(const WT* W, int N, int K, const float* x, const floa
   constexpr int OPG = EPI == GEMV_SWIGLU ? ROWS / 2 : ROWS;
   const int ngroups = (N + ROWS - 1) / ROWS, nw = grid * 4;
   const int max_out = (ngroups + nw - 1) / nw * OPG;
-  const size_t lds = ((size_t)K + 4 * (size_t)max_out) * sizeof(float);
+  constexpr bool Q8 = sizeof(WT) == 1;
+  if (Q8 && K % 32) return hipErrorInvalidValue;
+  const size_t lds = ((size_t)K + (Q8 ? K / 16 : 0) + 4 * (size_t)max_out) * sizeof(float);
+  const unsigned short* S =
+      Q8 ? reinterpret_cast<const unsigned short*>(reinterpret_cast<const char*>(W) +
+                                                   q8_scale_offset(N, K))
+         : nullptr;
   const int xr = K <= 8192 ? 1 : K <= 16384 ? 2 : 4;
 #define WICI_GEMV_GO(NR, XR)                                                                 \
   do {                                                                                       \
@@ -327,7 +386,7 @@ hipError_t launch_gemv_cfg(const WT* W, int N, int K, const float* x, const floa
       (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),                           \
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);       \
     launch_k(fn, dim3(grid), dim3(256), lds, st, kOnly, W, N, K, x, gain, eps, y, part,      \
-             max_out, rp);                                                                   \
+             max_out, rp, S);                                                                \
   } while (0)
 #define WICI_GEMV_XR(NR)                   \
   do {                                     \
@@ -361,10 +420,11 @@ template <typename WT, int EPI>
 static hipError_t gemv_dispatch(const GemvShape& s, const WT* W, int N, int K, const float* x,
                                 const float* gain, float eps, float* y, ArgmaxPart* part,
                                 hipStream_t st, const QkvRope* rope) {
-  // the same bytes per batch for both weight types
-  if (sizeof(WT) == 2)
-    return launch_gemv_cfg<WT, EPI, 2, 4>(W, N, K, x, gain, eps, y, part, s.grid, st, rope);
-  return launch_gemv_cfg<WT, EPI, 2, 2>(W, N, K, x, gain, eps, y, part, s.grid, st, rope);
+  // 16-byte loads per lane: 4 sweeps per batch for bf16 and Q8 (2 KiB of bf16 or
+  // 4 KiB of codes per row), 2 for fp32 (two loads per sweep)
+  if (sizeof(WT) == 4)
+    return launch_gemv_cfg<WT, EPI, 2, 2>(W, N, K, x, gain, eps, y, part, s.grid, st, rope);
+  return launch_gemv_cfg<WT, EPI, 2, 4>(W, N, K, x, gain, eps, y, part, s.grid, st, rope);
 }
 
 template <typename WT>
@@ -385,15 +445,22 @@ static hipError_t gemv_t(int epi, const WT* W, int N, int K, const float* x, con
 #undef WICI_GEMV_EPI
 }
 
-hipError_t launch_gemv(bool w_bf16, int epi, const void* W, int N, int K, const float* x,
+hipError_t launch_gemv(int wt, int epi, const void* W, int N, int K, const float* x,
                        const float* norm_gain, float eps, float* y, ArgmaxPart* part,
                        int* nblocks, hipStream_t st, const QkvRope* rope) {
   if (nblocks) *nblocks = gemv_shape(N, K).grid;
-  if (w_bf16)
-    return gemv_t<bf16_t>(epi, static_cast<const bf16_t*>(W), N, K, x, norm_gain, eps, y, part,
-                          st, rope);
-  return gemv_t<float>(epi, static_cast<const float*>(W), N, K, x, norm_gain, eps, y, part, st,
-                       rope);
+  switch (wt) {
+    case W_BF16:
+      return gemv_t<bf16_t>(epi, static_cast<const bf16_t*>(W), N, K, x, norm_gain, eps, y, part,
+                            st, rope);
+    case W_F32:
+      return gemv_t<float>(epi, static_cast<const float*>(W), N, K, x, norm_gain, eps, y, part,
+                           st, rope);
+    case W_Q8:
+      return gemv_t<uint8_t>(epi, static_cast<const uint8_t*>(W), N, K, x, norm_gain, eps, y,
+                             part, st, rope);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace wici

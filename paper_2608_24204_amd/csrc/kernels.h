@@ -8,6 +8,19 @@ namespace wici {
 
 enum GemvEpi { GEMV_STORE = 0, GEMV_RESID = 1, GEMV_SWIGLU = 2, GEMV_ARGMAX = 3, GEMV_QKV = 4 };
 
+// Weight storage (the values of the C ABI's wici_dtype).  A W_Q8 matrix [N, K]
+// is N*K code bytes (q + 128, row-major) followed, at the next 256-byte
+// boundary, by N*K/32 half-precision block scales (row-major, one per 32
+// consecutive weights of a row); the weight is (code - 128) * scale.
+enum WType { W_F32 = 0, W_BF16 = 1, W_Q8 = 2 };
+__host__ __device__ inline size_t q8_scale_offset(size_t n, size_t k) {
+  return (n * k + 255) / 256 * 256;
+}
+__host__ __device__ inline size_t weight_bytes(int wt, size_t n, size_t k) {
+  if (wt == W_Q8) return q8_scale_offset(n, k) + n * (k / 32) * 2;
+  return n * k * (wt == W_BF16 ? 2 : 4);
+}
+
 struct ArgmaxPart { float v; int32_t i; };
 
 // Timing of the decode launchers (used by the profiling entry point): while set
@@ -51,7 +64,7 @@ struct QkvRope {
 // (gate_i, up_i) and y[i] = silu(gate_i) * up_i.  ARGMAX: y[n] = acc and one
 // ArgmaxPart per block into `part` (grid size returned through *nblocks).
 // QKV: as described for QkvRope (`rope` required, N = (n_q + 2 n_kv) * hd).
-hipError_t launch_gemv(bool w_bf16, int epi, const void* W, int N, int K, const float* x,
+hipError_t launch_gemv(int wt, int epi, const void* W, int N, int K, const float* x,
                        const float* norm_gain, float eps, float* y, ArgmaxPart* part,
                        int* nblocks, hipStream_t st, const QkvRope* rope = nullptr);
 int gemv_argmax_blocks(int N);
@@ -67,7 +80,7 @@ hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int32
 
 // x[t, :] = E[tokens[t], :] for t < T (tokens == nullptr: the state's token, T = 1;
 // a negative state token, left by a failed step, gives a zero row).
-hipError_t launch_embed(bool w_bf16, const void* E, int d, const int32_t* tokens, int T,
+hipError_t launch_embed(int wt, const void* E, int V, int d, const int32_t* tokens, int T,
                         const void* state, float* x, hipStream_t st);
 // st->token = token and clear st->bad (a host-given token restarts decoding).
 hipError_t launch_set_token(void* state, int token, hipStream_t st);
@@ -106,7 +119,7 @@ bool attn_group_supported(int G);
 // written as an activation buffer).  A.nt == 0: vector fp32 product (W bf16 or
 // fp32); A.nt = 1..3: matrix-core product of the nt bf16 planes with bf16 W.
 // K must be a multiple of 32.
-hipError_t launch_gemm(bool w_bf16, int epi, const ActBuf& A, int lda, const void* W, int M,
+hipError_t launch_gemm(int wt, int epi, const ActBuf& A, int lda, const void* W, int M,
                        int N, int K, float* C, int ldc, const ActBuf& H, int ldh,
                        hipStream_t st);
 

@@ -14,17 +14,31 @@ void set_launch_timer(const LaunchTimer* t) { g_launch_timer = t; }
 const LaunchTimer* launch_timer() { return g_launch_timer; }
 
 // ---- embedding ------------------------------------------------------------------
+// Q8 rows: codes (q + 128) and one half-precision scale per 32 elements (S).
+__device__ __forceinline__ void load8(const uint8_t* p, float* o, const unsigned short* s) {
+  const uint2 c = *reinterpret_cast<const uint2*>(p);
+  const float d = (float)__builtin_bit_cast(_Float16, *s);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    o[j] = ((float)((c.x >> (8 * j)) & 0xffu) - 128.f) * d;
+    o[4 + j] = ((float)((c.y >> (8 * j)) & 0xffu) - 128.f) * d;
+  }
+}
+
 template <typename WT>
-__global__ __launch_bounds__(256) void k_embed(const WT* __restrict__ E, int d,
+__global__ __launch_bounds__(256) void k_embed(const WT* __restrict__ E,
+                                               const unsigned short* __restrict__ S, int d,
                                                const int32_t* __restrict__ tokens,
                                                const DecodeState* __restrict__ st,
                                                float* __restrict__ x) {
   const int t = blockIdx.x;
   const int tok = tokens ? tokens[t] : st->token;
-  const WT* row = E + (size_t)(tok < 0 ? 0 : tok) * d;
+  const size_t r = (size_t)(tok < 0 ? 0 : tok);
+  const WT* row = E + r * d;
   for (int k = threadIdx.x * 8; k < d; k += 256 * 8) {
     float v[8];
-    load8(row + k, v);
+    if constexpr (sizeof(WT) == 1) load8(row + k, v, S + r * (d / 32) + k / 32);
+    else load8(row + k, v);
     if (tok < 0)
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = 0.f;
@@ -34,15 +48,27 @@ __global__ __launch_bounds__(256) void k_embed(const WT* __restrict__ E, int d,
   }
 }
 
-hipError_t launch_embed(bool w_bf16, const void* E, int d, const int32_t* tokens, int T,
+hipError_t launch_embed(int wt, const void* E, int V, int d, const int32_t* tokens, int T,
                         const void* state, float* x, hipStream_t st) {
   const DecodeState* s = static_cast<const DecodeState*>(state);
-  if (w_bf16)
-    launch_k(k_embed<bf16_t>, dim3(T), dim3(256), 0, st, kOnly,
-                       static_cast<const bf16_t*>(E), d, tokens, s, x);
-  else
-    launch_k(k_embed<float>, dim3(T), dim3(256), 0, st, kOnly,
-                       static_cast<const float*>(E), d, tokens, s, x);
+  switch (wt) {
+    case W_BF16:
+      launch_k(k_embed<bf16_t>, dim3(T), dim3(256), 0, st, kOnly, static_cast<const bf16_t*>(E),
+               (const unsigned short*)nullptr, d, tokens, s, x);
+      break;
+    case W_F32:
+      launch_k(k_embed<float>, dim3(T), dim3(256), 0, st, kOnly, static_cast<const float*>(E),
+               (const unsigned short*)nullptr, d, tokens, s, x);
+      break;
+    case W_Q8: {
+      const uint8_t* c = static_cast<const uint8_t*>(E);
+      launch_k(k_embed<uint8_t>, dim3(T), dim3(256), 0, st, kOnly, c,
+               reinterpret_cast<const unsigned short*>(c + q8_scale_offset(V, d)), d, tokens, s,
+               x);
+      break;
+    }
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -18,6 +18,9 @@
 
 using wici::ArgmaxPart;
 using wici::DecodeState;
+static_assert((int)wici::W_F32 == WICI_F32 && (int)wici::W_BF16 == WICI_BF16 &&
+                  (int)wici::W_Q8 == WICI_Q8,
+              "kernel weight types follow wici_dtype");
 
 namespace {
 
@@ -59,7 +62,8 @@ bool config_ok(const wici_config* c, std::string* why) {
   if (c->vocab < 1) return bad("vocab must be >= 1");
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return bad("rms_eps must be > 0");
   if (!(c->rope_base > 1.0) || !std::isfinite(c->rope_base)) return bad("rope_base must be > 1");
-  if (c->weight_dtype != WICI_F32 && c->weight_dtype != WICI_BF16) return bad("bad weight_dtype");
+  if (c->weight_dtype != WICI_F32 && c->weight_dtype != WICI_BF16 && c->weight_dtype != WICI_Q8)
+    return bad("bad weight_dtype");
   if (c->kv_dtype != WICI_F32 && c->kv_dtype != WICI_BF16) return bad("bad kv_dtype");
   if (c->max_seq < 1 || c->max_seq > (1 << 20)) return bad("max_seq out of range");
   if (c->prefill_chunk < 1 || c->prefill_chunk > 8192) return bad("prefill_chunk out of range");
@@ -76,24 +80,26 @@ bool config_ok(const wici_config* c, std::string* why) {
 
 Layout make_layout(const wici_config& c) {
   Layout L{};
-  const size_t ws = dsize(c.weight_dtype), d = c.d_model, F = c.ffn_dim, V = c.vocab;
+  const int wt = c.weight_dtype;
+  const size_t d = c.d_model, F = c.ffn_dim, V = c.vocab;
   const size_t qd = (size_t)c.n_heads * c.head_dim, kvd = (size_t)c.n_kv_heads * c.head_dim;
   const size_t nqkv = qd + 2 * kvd;
+  auto mat = [&](size_t n, size_t k) { return wici::weight_bytes(wt, n, k); };
   size_t o = 0;
-  L.l_wqkv = o; o = align_up(o + nqkv * d * ws);
-  L.l_wo = o; o = align_up(o + d * qd * ws);
-  L.l_wgu = o; o = align_up(o + 2 * F * d * ws);
-  L.l_wdown = o; o = align_up(o + d * F * ws);
+  L.l_wqkv = o; o = align_up(o + mat(nqkv, d));
+  L.l_wo = o; o = align_up(o + mat(d, qd));
+  L.l_wgu = o; o = align_up(o + mat(2 * F, d));
+  L.l_wdown = o; o = align_up(o + mat(d, F));
   L.l_anorm = o; o = align_up(o + d * 4);
   L.l_fnorm = o; o = align_up(o + d * 4);
   L.layer_stride = o;
   o = L.layer_stride * c.n_layers;
-  L.embed = o; o = align_up(o + V * d * ws);
+  L.embed = o; o = align_up(o + mat(V, d));
   L.final_norm = o; o = align_up(o + d * 4);
   if (c.tied_embeddings) {
     L.lm_head = L.embed;
   } else {
-    L.lm_head = o; o = align_up(o + V * d * ws);
+    L.lm_head = o; o = align_up(o + mat(V, d));
   }
   const size_t half = c.head_dim / 2;
   L.rope_cos = o; o = align_up(o + (size_t)c.max_seq * half * 4);
@@ -233,7 +239,8 @@ bool usable(const wici_model* m) { return m && !m->failed; }
 hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers = nullptr) {
   const wici_config& c = m->cfg;
   const Layout& L = m->L;
-  const bool wb = c.weight_dtype == WICI_BF16, kb = c.kv_dtype == WICI_BF16;
+  const int wb = c.weight_dtype;
+  const bool kb = c.kv_dtype == WICI_BF16;
   const int d = c.d_model, F = c.ffn_dim, qd = c.n_heads * c.head_dim;
   const int nqkv = qd + 2 * c.n_kv_heads * c.head_dim;
   float* x = m->S<float>(L.x);
@@ -263,7 +270,7 @@ hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers 
     disarm();                   \
     if (e) return e;            \
   } while (0)
-  WICI_STEP(wici::launch_embed(wb, m->dw + L.embed, d, nullptr, 1, st, x, s));
+  WICI_STEP(wici::launch_embed(wb, m->dw + L.embed, c.vocab, d, nullptr, 1, st, x, s));
   for (int l = 0; l < c.n_layers; ++l) {
     wici::QkvRope rope{};
     rope.cos_t = m->W<float>(L.rope_cos);
@@ -301,7 +308,8 @@ hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers 
 hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   const wici_config& c = m->cfg;
   const Layout& L = m->L;
-  const bool wb = c.weight_dtype == WICI_BF16, kb = c.kv_dtype == WICI_BF16;
+  const int wb = c.weight_dtype;
+  const bool kb = c.kv_dtype == WICI_BF16;
   const int d = c.d_model, F = c.ffn_dim, qd = c.n_heads * c.head_dim;
   const int nqkv = qd + 2 * c.n_kv_heads * c.head_dim;
   float* x = m->S<float>(L.x);
@@ -322,7 +330,8 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   const wici::ActBuf none{};
   hipStream_t s = m->stream;
   hipError_t e;
-  if ((e = wici::launch_embed(wb, m->dw + L.embed, d, m->S<int32_t>(L.tokens), T, nullptr, x, s)))
+  if ((e = wici::launch_embed(wb, m->dw + L.embed, c.vocab, d, m->S<int32_t>(L.tokens), T, nullptr,
+                              x, s)))
     return e;
   for (int l = 0; l < c.n_layers; ++l) {
     if ((e = wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, T, d,
@@ -478,7 +487,9 @@ wici_status wici_load_weights(wici_model* m, const wici_tensor* tensors, int32_t
     const TensorSpec& sp = m->specs[it->second];
     if (seen[it->second]) return fail(m, WICI_E_ARG, "tensor '%s' given twice", t.name);
     seen[it->second] = 1;
-    if (t.dtype != sp.dtype) return fail(m, WICI_E_ARG, "tensor '%s': wrong dtype", t.name);
+    const bool dtype_ok = sp.dtype == WICI_Q8 ? (t.dtype == WICI_BF16 || t.dtype == WICI_F32)
+                                              : t.dtype == sp.dtype;
+    if (!dtype_ok) return fail(m, WICI_E_ARG, "tensor '%s': wrong dtype", t.name);
     const bool shape_ok = sp.ndim == 1 ? (t.ndim == 1 && t.shape[0] == sp.rows)
                                        : (t.ndim == 2 && t.shape[0] == sp.rows && t.shape[1] == sp.cols);
     if (!shape_ok) return fail(m, WICI_E_ARG, "tensor '%s': wrong shape", t.name);
@@ -489,9 +500,64 @@ wici_status wici_load_weights(wici_model* m, const wici_tensor* tensors, int32_t
   const Layout& L = m->L;
   const size_t ws = dsize(c.weight_dtype), d = c.d_model;
   const size_t qd = (size_t)c.n_heads * c.head_dim, kvd = (size_t)c.n_kv_heads * c.head_dim;
+  if (c.weight_dtype == WICI_Q8) {
+    // quantise every matrix first (host), so a bad tensor uploads nothing
+    std::vector<std::vector<uint8_t>> codes(n_tensors);
+    std::vector<std::vector<uint16_t>> scales(n_tensors);
+    for (int i = 0; i < n_tensors; ++i) {
+      const wici_tensor& t = tensors[i];
+      const TensorSpec& sp = m->specs[idx[i]];
+      if (sp.dtype != WICI_Q8) continue;
+      const size_t n = (size_t)sp.rows * sp.cols, es = dsize(t.dtype);
+      std::vector<char> host;
+      const void* src = t.data;
+      if (t.on_device) {
+        host.resize(n * es);
+        HIP_TRY(m, hipMemcpy(host.data(), t.data, n * es, hipMemcpyDeviceToHost));
+        src = host.data();
+      }
+      codes[i].resize(n);
+      scales[i].resize(n / 32);
+      if (wici_quantize_q8(src, t.dtype, sp.rows, sp.cols, codes[i].data(), scales[i].data()) !=
+          WICI_OK)
+        return fail(m, WICI_E_ARG, "tensor '%s': non-finite weight or scale overflow", t.name);
+    }
+    for (int i = 0; i < n_tensors; ++i) {
+      const wici_tensor& t = tensors[i];
+      const TensorSpec& sp = m->specs[idx[i]];
+      if (sp.dtype != WICI_Q8) continue;
+      // region of the packed matrix, its row count and width, this tensor's first
+      // row and row step (2 for the interleaved gate/up rows)
+      size_t base = 0, rows = sp.rows, r0 = 0, step = 1;
+      const size_t K = sp.cols;
+      switch (sp.kind) {
+        case T_EMBED: base = L.embed; break;
+        case T_LM_HEAD: base = L.lm_head; break;
+        case T_WQ: base = m->layer(sp.layer, L.l_wqkv); rows = qd + 2 * kvd; break;
+        case T_WK: base = m->layer(sp.layer, L.l_wqkv); rows = qd + 2 * kvd; r0 = qd; break;
+        case T_WV: base = m->layer(sp.layer, L.l_wqkv); rows = qd + 2 * kvd; r0 = qd + kvd; break;
+        case T_WO: base = m->layer(sp.layer, L.l_wo); break;
+        case T_DOWN: base = m->layer(sp.layer, L.l_wdown); break;
+        case T_GATE:
+        case T_UP:
+          base = m->layer(sp.layer, L.l_wgu); rows = 2 * (size_t)sp.rows;
+          r0 = sp.kind == T_UP ? 1 : 0; step = 2;
+          break;
+        default: return fail(m, WICI_E_ARG, "tensor '%s': not a matrix", t.name);
+      }
+      char* dc = m->dw + base;
+      char* dsc = dc + wici::q8_scale_offset(rows, K);
+      const size_t sb = K / 32 * 2;  // scale bytes per row
+      HIP_TRY(m, hipMemcpy2D(dc + r0 * K, step * K, codes[i].data(), K, K, (size_t)sp.rows,
+                             hipMemcpyHostToDevice));
+      HIP_TRY(m, hipMemcpy2D(dsc + r0 * sb, step * sb, scales[i].data(), sb, sb, (size_t)sp.rows,
+                             hipMemcpyHostToDevice));
+    }
+  }
   for (int i = 0; i < n_tensors; ++i) {
     const wici_tensor& t = tensors[i];
     const TensorSpec& sp = m->specs[idx[i]];
+    if (sp.dtype == WICI_Q8) continue;
     const hipMemcpyKind kind = t.on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
     const size_t es = dsize(sp.dtype);
     const size_t bytes = (size_t)sp.rows * sp.cols * es;
@@ -551,7 +617,7 @@ wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
     last_T = T;
   }
   int nb = 0;
-  const bool wb = c.weight_dtype == WICI_BF16;
+  const int wb = c.weight_dtype;
   HIP_TRY(m, wici::launch_gemv(wb, wici::GEMV_ARGMAX, m->dw + L.lm_head, c.vocab, c.d_model,
                                m->S<float>(L.x) + (size_t)(last_T - 1) * c.d_model,
                                m->W<float>(L.final_norm), c.rms_eps, m->S<float>(L.logits),

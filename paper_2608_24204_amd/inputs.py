@@ -86,7 +86,7 @@ def _fill_block(cfg, tidx, b, flat_out, is_bf16, seed):
 def make_weights(cfg: ModelConfig, seed: int = WEIGHT_SEED, gain_std: float = 0.0,
                  threads: int | None = None) -> dict[str, np.ndarray]:
     """All weight tensors of ``cfg`` by name (see module docstring for the recipe)."""
-    is_bf16 = cfg.weight_dtype == "bf16"
+    is_bf16 = cfg.weight_dtype in ("bf16", "q8")   # q8 models start from bf16 weights
     out: dict[str, np.ndarray] = {}
     jobs = []
     for tidx, (name, shape, kind) in enumerate(tensor_specs(cfg)):
@@ -124,7 +124,7 @@ def weights_f64(cfg: ModelConfig, weights: dict[str, np.ndarray],
                 threads: int | None = None) -> dict[str, np.ndarray]:
     """The exact values of the stored weights as float64 arrays (storage decoding
     only: a bf16 bit pattern is widened, never re-rounded)."""
-    is_bf16 = cfg.weight_dtype == "bf16"
+    is_bf16 = cfg.weight_dtype in ("bf16", "q8")   # q8 models start from bf16 weights
 
     def conv(item):
         name, a = item

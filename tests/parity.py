@@ -17,7 +17,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-from oracle import DecoderOracle
+from oracle import DecoderOracle, dequantize_q8, quantize_q8
 
 
 def oracle_step_logits(cfg, w64, prompt, ids, kv_round=None) -> np.ndarray:
@@ -68,3 +68,32 @@ def compare(gpu_ids, gpu_logits, ora_logits) -> ParityReport:
             if err is not None and margin <= 2 * err:
                 rep.near_ties.append((s, margin, 2 * err))
     return rep
+
+
+class LazyQ8F64:
+    """Oracle weights of a block-scaled 8-bit model: each matrix (bf16 bits or
+    float32) quantised by the oracle's own rule and dequantised to float64 when
+    first asked for (norm gains are passed through); one tensor at a time, so a
+    full-size model fits in host memory."""
+
+    def __init__(self, weights):
+        self.w = weights
+
+    def _f32(self, a):
+        a = np.asarray(a)
+        if a.dtype == np.uint16:
+            return (a.astype(np.uint32) << 16).view(np.float32)
+        return a.astype(np.float32)
+
+    def __getitem__(self, name):
+        a = self._f32(self.w[name])
+        if a.ndim == 2:
+            q, d = quantize_q8(a)
+            return dequantize_q8(q, d)
+        return a.astype(np.float64)
+
+    def __contains__(self, name):
+        return name in self.w
+
+    def keys(self):
+        return self.w.keys()

@@ -6,9 +6,10 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
-from paper_2608_24204_amd import binding, configs
+from paper_2608_24204_amd import binding, configs, inputs
 from tests.helpers import small_cfg
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -20,7 +21,7 @@ pytestmark = pytest.mark.skipif(not os.path.exists(binding.LIB_PATH),
 def test_every_declared_symbol_is_exported():
     lib = binding.load_library()
     header = open(os.path.join(ROOT, "include", "wici.h")).read()
-    declared = set(re.findall(r"\b(wici_[a-z_]+)\s*\(", header))
+    declared = set(re.findall(r"\b(wici_[a-z0-9_]+)\s*\(", header))
     assert declared == set(binding.EXPORTED)
     for name in declared:
         assert hasattr(lib, name), name
@@ -123,3 +124,46 @@ def test_tensor_array_marshalling():
     assert arr[0].name == b"tok_embeddings" and arr[0].dtype == binding.WICI_BF16
     assert arr[0].ndim == 2 and tuple(arr[0].shape) == (100, 256) and arr[0].on_device == 0
     assert arr[1].dtype == binding.WICI_F32 and arr[1].ndim == 1 and arr[1].shape[0] == 256
+
+
+def test_library_quantiser_matches_oracle_bit_for_bit():
+    """wici_quantize_q8 (host C++) against the oracle's float32 rule: identical codes
+    and identical half-precision scale bits, on bf16 and float32 input, including
+    ties, zero blocks, subnormal and rounding-boundary scales."""
+    from oracle import quantize_q8 as oracle_q8
+    rng = np.random.default_rng(11)
+    w = (rng.standard_normal((48, 256)) * 0.02).astype(np.float32)
+    w[0, :32] = 0.0
+    w[1, 32:64] *= 1e-6                                   # subnormal half scales
+    w[2, :32] = np.arange(32, dtype=np.float32) - 15.5     # exact half-way ratios
+    w[3, :32] = (np.arange(32) % 7 - 3).astype(np.float32) * np.float32(2.0 ** -7)
+    w[4, :32] = 1e-9                                      # scale rounds to zero
+    w[5, 64:96] = rng.standard_normal(32).astype(np.float32) * 1000.0
+    bits = np.empty(w.shape, np.uint16)
+    inputs.f32_to_bf16_bits(w, bits)
+    for src in (w, bits):
+        ref_in = w if src.dtype == np.float32 else inputs.bf16_bits_to_f32(bits)
+        q, d = oracle_q8(ref_in)
+        codes, scales = binding.quantize_q8(src)
+        assert np.array_equal(codes.astype(np.int16) - 128, q.astype(np.int16))
+        assert np.array_equal(scales.view(np.uint16), d.view(np.uint16))
+    # a random sweep over many magnitudes (scale rounding in every binade)
+    w2 = (rng.standard_normal((64, 512)) * np.exp(rng.uniform(-20, 5, (64, 1)))).astype(np.float32)
+    q, d = oracle_q8(w2)
+    codes, scales = binding.quantize_q8(w2)
+    assert np.array_equal(codes.astype(np.int16) - 128, q.astype(np.int16))
+    assert np.array_equal(scales.view(np.uint16), d.view(np.uint16))
+
+
+def test_library_quantiser_rejects_bad_input():
+    lib = binding.load_library()
+    buf = np.zeros((2, 64), np.float32)
+    codes = np.empty((2, 64), np.uint8)
+    scales = np.empty((2, 2), np.uint16)
+    assert lib.wici_quantize_q8(buf.ctypes.data, binding.WICI_F32, 2, 48, codes.ctypes.data,
+                                scales.ctypes.data) == binding.WICI_E_ARG
+    assert lib.wici_quantize_q8(buf.ctypes.data, 7, 2, 64, codes.ctypes.data,
+                                scales.ctypes.data) == binding.WICI_E_ARG
+    buf[1, 5] = np.nan
+    assert lib.wici_quantize_q8(buf.ctypes.data, binding.WICI_F32, 2, 64, codes.ctypes.data,
+                                scales.ctypes.data) == binding.WICI_E_ARG

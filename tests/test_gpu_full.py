@@ -4,8 +4,10 @@ times) on the GPU, against the float64 oracle's logits at every generated step
 (the oracle runs once over prompt + generated ids with all positions' logits, so
 each step is teacher-forced on the GPU's own ids).
 
-The 1B- and 8B-shaped configurations run by default; the long-context 8B and the
-32B shapes (minutes of float64 host work each) run when WICI_FULL_PARITY=all."""
+The 1B- and 8B-shaped configurations run by default, with bf16 weights and with
+block-scaled 8-bit weights (the oracle then runs on its own quantisation of the
+same bf16 weights); the long-context 8B and the 32B shapes (minutes of float64
+host work each) run when WICI_FULL_PARITY=all."""
 
 from __future__ import annotations
 
@@ -18,12 +20,12 @@ import pytest
 
 from oracle import DecoderOracle
 from paper_2608_24204_amd import configs, inputs
-from tests.parity import compare
+from tests.parity import LazyQ8F64, compare
 
 pytestmark = pytest.mark.gpu
 
-DEFAULT = ["1b", "8b"]
-OPT_IN = ["8b_long", "32b"]
+DEFAULT = ["1b", "8b", "1b_q8", "8b_q8"]
+OPT_IN = ["8b_long", "32b", "32b_q8"]
 SELECTED = DEFAULT + (OPT_IN if os.environ.get("WICI_FULL_PARITY") == "all" else [])
 MODES = os.environ.get("WICI_FULL_PARITY_MODES", "bf16x3").split(",")
 
@@ -57,7 +59,8 @@ def test_full_size_greedy_run_matches_oracle(cuda_ok, name, mode):
         m.close()
     t1 = time.time()
     seq = np.concatenate([prompt, np.asarray(ids[:-1])])
-    orc = DecoderOracle(cfg, inputs.LazyF64(w), max_seq=len(seq))
+    w64 = LazyQ8F64(w) if cfg.weight_dtype == "q8" else inputs.LazyF64(w)
+    orc = DecoderOracle(cfg, w64, max_seq=len(seq))
     print(f"[full parity] {name}: GPU run done in {t1 - t0:.1f} s; oracle over {len(seq)} "
           f"positions", flush=True)
     ora = orc.forward(seq, all_logits=True, first_row=len(prompt) - 1,
