@@ -126,6 +126,66 @@ def cpu_baseline(cfg, w, n_prompt, n_decode):
     return out, (prompt, ids, logs)
 
 
+def model_cache_sweep(cfg_name, store_root, thresholds_mib):
+    """Model load time against the caching threshold (the paper's model-caching
+    figure): per threshold, the caller's MD5 time over the tensors at or above it,
+    a cold load into an empty store (hash, upload, save), a warm load sending only
+    those hashes (store reads + upload), the bytes the caller still sends, and a
+    plain upload for reference.  Prints one JSON line."""
+    import shutil
+
+    import torch
+
+    from paper_2608_24204_amd import binding, configs, inputs
+    cfg = configs.CONFIGS[cfg_name]
+    w = inputs.make_weights(cfg)
+    total = sum(a.nbytes for a in w.values())
+    rows = []
+
+    def fresh():
+        return binding.WiciModel(cfg, max_seq=64)
+
+    m = fresh()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    m.load_weights(w)
+    plain_s = time.perf_counter() - t0
+    m.close()
+    for t_mib in thresholds_mib:
+        thr = int(t_mib * 2 ** 20)
+        store = os.path.join(store_root, f"wici_store_{t_mib}")
+        shutil.rmtree(store, ignore_errors=True)
+        os.makedirs(store)
+        big = [n for n, a in w.items() if a.nbytes >= thr]
+        t0 = time.perf_counter()
+        hashes = {n: binding.md5(w[n]) for n in big}
+        hash_s = time.perf_counter() - t0
+        m = fresh()
+        t0 = time.perf_counter()
+        out = m.load_weights_cached(w, store, thr)
+        cold_s = time.perf_counter() - t0
+        m.close()
+        m = fresh()
+        t0 = time.perf_counter()
+        out2 = m.load_weights_cached(w, store, thr, hashes=hashes)
+        warm_s = time.perf_counter() - t0
+        m.close()
+        sent = sum(w[n].nbytes for n in w if n not in hashes)
+        rows.append({"threshold_mib": t_mib, "hashed_tensors": len(big),
+                     "hash_s": hash_s, "cold_load_s": cold_s,
+                     "warm_load_s": warm_s, "warm_total_s": hash_s + warm_s,
+                     "bytes_sent_warm": sent,
+                     "hits": sum(o == binding.WICI_CACHE_HIT for o in out2.values()),
+                     "saved_cold": sum(o == binding.WICI_CACHE_SAVED for o in out.values())})
+        log(f"threshold {t_mib} MiB: {len(big)} hashed, hash {hash_s:.2f} s, cold "
+            f"{cold_s:.2f} s, warm {warm_s:.2f} s, caller sends {sent / 1e6:.1f} MB")
+        shutil.rmtree(store, ignore_errors=True)
+    print(json.dumps({"metric": "model load time vs caching threshold", "config": cfg_name,
+                      "tensors": len(w), "model_bytes": total, "plain_load_s": plain_s,
+                      "rows": rows}), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,7 +201,14 @@ def main(argv=None):
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before the timed region, copy MIB MiB device-to-device (a plain "
                          "copy of known size, for calibrating memory counters)")
+    ap.add_argument("--model-cache", action="store_true",
+                    help="instead of the benchmark: model load time against the caching "
+                         "threshold (store under --store-root)")
+    ap.add_argument("--store-root", default=os.environ.get("TMPDIR", "/tmp"))
     args = ap.parse_args(argv)
+    if args.model_cache:
+        return model_cache_sweep(args.config, args.store_root,
+                                 [0, 0.0625, 1, 16, 64, 256, 4096])
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(this build has no multi-GPU path)", file=sys.stderr)

@@ -220,6 +220,37 @@ wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* n
 wici_status wici_quantize_q8(const void* src, int32_t src_dtype, int64_t rows, int64_t cols,
                              uint8_t* codes, uint16_t* scales);
 
+/* MD5 (RFC 1321) of `bytes` bytes of host memory into out16: the name of a
+ * tensor in the content store of wici_load_weights_cached.  Host only. */
+wici_status wici_md5(const void* data, size_t bytes, uint8_t* out16);
+
+/* What wici_load_weights_cached did with each tensor. */
+enum {
+  WICI_CACHE_SENT = 0,   /* below the threshold: uploaded from the given data */
+  WICI_CACHE_HIT = 1,    /* found in the store: uploaded from the store's file */
+  WICI_CACHE_SAVED = 2,  /* not in the store: uploaded from the data, then saved */
+  WICI_CACHE_NEEDED = 3  /* not in the store and no data given: not uploaded */
+};
+
+/* Weight upload through a content-addressed store, the paper's model caching
+ * (Sec. "Model Caching"): a tensor of at least threshold_bytes is named by the
+ * MD5 of its bytes (hashes[16*i], or computed from its data when hashes is
+ * NULL); if store_dir holds a file of that name (and of the tensor's size) the
+ * tensor is loaded from it and its data pointer is not read, else it is uploaded
+ * from its data and written to the store (written to a temporary name, then
+ * renamed).  A tensor below the threshold is always uploaded from its data.  A
+ * caller that has sent only hashes (data NULL) gets WICI_CACHE_NEEDED for the
+ * misses and sends those tensors again with data, as in the paper's exchange.
+ * outcome[i] receives one WICI_CACHE_* value per tensor.  Uploading follows
+ * wici_load_weights (same names, shapes, dtypes, errors).  Errors: WICI_E_ARG
+ * (NULL model/store_dir/outcome, a negative threshold, a bad shape, data NULL
+ * where it is needed), anything wici_load_weights returns; a store file that
+ * cannot be written is not an error. */
+wici_status wici_load_weights_cached(wici_model* m, const wici_tensor* tensors,
+                                     const uint8_t* hashes, int32_t n_tensors,
+                                     const char* store_dir, int64_t threshold_bytes,
+                                     int32_t* outcome);
+
 /* Message of the last failed call on this model ("" if none).  Valid until the
  * next call on the model. */
 const char* wici_last_error(const wici_model* m);

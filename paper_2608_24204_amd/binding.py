@@ -28,8 +28,8 @@ WICI_FLAG_NO_GRAPH = 1
 # every entry point include/wici.h declares
 EXPORTED = ["wici_create", "wici_memory_requirements", "wici_bind_memory", "wici_load_weights",
             "wici_prefill", "wici_decode_step", "wici_decode_n", "wici_reset_kv", "wici_position",
-            "wici_read_kv", "wici_profile_decode_step", "wici_quantize_q8", "wici_last_error",
-            "wici_destroy"]
+            "wici_read_kv", "wici_profile_decode_step", "wici_quantize_q8", "wici_md5",
+            "wici_load_weights_cached", "wici_last_error", "wici_destroy"]
 
 
 class WiciConfig(ctypes.Structure):
@@ -85,6 +85,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
         "wici_profile_decode_step": ([P, i32, ctypes.POINTER(i32), P, i32, ctypes.POINTER(i32)],
                                      ctypes.c_int),
         "wici_quantize_q8": ([P, i32, ctypes.c_int64, ctypes.c_int64, P, P], ctypes.c_int),
+        "wici_md5": ([P, sz, P], ctypes.c_int),
+        "wici_load_weights_cached": ([P, ctypes.POINTER(WiciTensor), P, i32, ctypes.c_char_p,
+                                      ctypes.c_int64, P], ctypes.c_int),
         "wici_last_error": ([P], ctypes.c_char_p),
         "wici_destroy": ([P], None),
     }
@@ -132,6 +135,20 @@ def quantize_q8(w: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
     if st != WICI_OK:
         raise WiciError(st, "wici_quantize_q8")
     return codes, scales.view(np.float16)
+
+
+WICI_CACHE_SENT, WICI_CACHE_HIT, WICI_CACHE_SAVED, WICI_CACHE_NEEDED = 0, 1, 2, 3
+
+
+def md5(data) -> bytes:
+    """The library's MD5 (wici_md5) of a numpy array's bytes."""
+    lib = load_library()
+    a = np.ascontiguousarray(data)
+    out = (ctypes.c_uint8 * 16)()
+    st = lib.wici_md5(a.ctypes.data if a.nbytes else None, a.nbytes, out)
+    if st != WICI_OK:
+        raise WiciError(st, "wici_md5")
+    return bytes(out)
 
 
 def memory_requirements(c: WiciConfig) -> tuple[int, int, int]:
@@ -222,6 +239,41 @@ class WiciModel:
         arr, keep = tensor_array(self.cfg, weights)
         self._check(self.lib.wici_load_weights(self.h, arr, len(weights)), "wici_load_weights")
         del keep
+
+    def load_weights_cached(self, weights: Mapping[str, object], store_dir: str,
+                            threshold_bytes: int = 0, hashes: Mapping[str, bytes] | None = None):
+        """Upload through the content store (wici_load_weights_cached).  With `hashes`
+        (name -> 16-byte MD5), tensors named there are sent as hashes only (no data);
+        returns {name: WICI_CACHE_* outcome}."""
+        names = list(weights)
+        if hashes is not None:
+            send = {n: (None if n in hashes else weights[n]) for n in names}
+        else:
+            send = weights
+        arr, keep = tensor_array(self.cfg, {n: (weights[n] if send[n] is None else send[n])
+                                            for n in names})
+        if hashes is not None:
+            for i, n in enumerate(names):
+                if n in hashes:
+                    arr[i].data = None
+        hb = None
+        if hashes is not None:
+            # the library reads the hash of every tensor at or above the threshold:
+            # those not given are hashed here from their data (the caller's side of
+            # the exchange); smaller tensors are always sent and need none
+            hb = np.zeros((len(names), 16), np.uint8)
+            for i, n in enumerate(names):
+                h = hashes.get(n)
+                if h is None and np.asarray(weights[n]).nbytes >= threshold_bytes:
+                    h = md5(weights[n])
+                if h is not None:
+                    hb[i] = np.frombuffer(h, np.uint8)
+        out = np.zeros(len(names), np.int32)
+        self._check(self.lib.wici_load_weights_cached(
+            self.h, arr, hb.ctypes.data if hb is not None else None, len(names),
+            store_dir.encode(), int(threshold_bytes), out.ctypes.data), "wici_load_weights_cached")
+        del keep
+        return {n: int(o) for n, o in zip(names, out)}
 
     def prefill(self, tokens, want_logits: bool = False):
         toks = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32).reshape(-1))

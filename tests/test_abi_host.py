@@ -167,3 +167,51 @@ def test_library_quantiser_rejects_bad_input():
     buf[1, 5] = np.nan
     assert lib.wici_quantize_q8(buf.ctypes.data, binding.WICI_F32, 2, 64, codes.ctypes.data,
                                 scales.ctypes.data) == binding.WICI_E_ARG
+
+
+# MD5 test suite of RFC 1321 (appendix A.5)
+RFC1321 = [
+    (b"", "d41d8cd98f00b204e9800998ecf8427e"),
+    (b"a", "0cc175b9c0f1b6a831c399e269772661"),
+    (b"abc", "900150983cd24fb0d6963f7d28e17f72"),
+    (b"message digest", "f96b697d7cb7938d525a2f31aaf161d0"),
+    (b"abcdefghijklmnopqrstuvwxyz", "c3fcd3d76192e4007dfb496cca67e13b"),
+    (b"ABCDEFGHIJKLMNOPQRSTUVWXYZabcdefghijklmnopqrstuvwxyz0123456789",
+     "d174ab98d277d9f5a5611c2c9f419d9f"),
+    (b"1234567890" * 8, "57edf4a22be3c955ac49da2e2107b67a"),
+]
+
+
+@pytest.mark.parametrize("msg,digest", RFC1321)
+def test_md5_rfc1321_suite(msg, digest):
+    assert binding.md5(np.frombuffer(msg, np.uint8)).hex() == digest
+
+
+def test_md5_lengths_around_block_boundaries():
+    import hashlib
+    rng = np.random.default_rng(3)
+    for n in [1, 55, 56, 57, 63, 64, 65, 119, 120, 127, 128, 129, 1000, 4096, 100003]:
+        a = rng.integers(0, 256, n, dtype=np.uint8)
+        assert binding.md5(a) == hashlib.md5(a.tobytes()).digest(), n
+
+
+def test_cached_load_checks_arguments():
+    lib = binding.load_library()
+    out = (ctypes.c_int32 * 1)()
+    assert lib.wici_load_weights_cached(None, None, None, 0, b"/tmp", 0, out) == binding.WICI_E_ARG
+    c = _cfg()
+    h = ctypes.c_void_p()
+    assert lib.wici_create(ctypes.byref(c), None, ctypes.byref(h)) == binding.WICI_OK
+    try:
+        t = (binding.WiciTensor * 1)()
+        t[0].name = b"norm"
+        t[0].dtype = binding.WICI_F32
+        t[0].ndim = 1
+        t[0].shape[0] = c.d_model
+        t[0].data = None
+        # below the threshold a tensor must carry data
+        assert lib.wici_load_weights_cached(h, t, None, 1, b"/tmp", 1 << 30, out) == binding.WICI_E_ARG
+        assert lib.wici_load_weights_cached(h, t, None, 1, None, 0, out) == binding.WICI_E_ARG
+        assert lib.wici_load_weights_cached(h, t, None, 1, b"/tmp", -1, out) == binding.WICI_E_ARG
+    finally:
+        lib.wici_destroy(h)
