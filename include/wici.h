@@ -175,6 +175,39 @@ wici_status wici_decode_step(wici_model* m, int32_t token_in, int32_t* next_toke
 wici_status wici_decode_n(wici_model* m, int32_t token_in, int32_t n, int32_t* tokens_out,
                           int32_t* n_done, float* logits);
 
+/* Bind a second client to the weights of `src` (the paper's multi-client
+ * setting, Sec. "WiCi Library", context management: one model per client, all
+ * on the same GPU): m uses src's weight memory read-only (non-owning; src must
+ * stay alive and must not reload weights while m is used) and its own KV cache
+ * and scratch (sizes from wici_memory_requirements of m's configuration).  The
+ * configurations must agree on everything the weight region depends on (shapes,
+ * weight dtype, rms_eps, rope_base, tied_embeddings, max_seq).  m becomes ready
+ * at once; wici_load_weights on m is refused (WICI_E_STATE).  Allowed once, in
+ * the created state; resets the KV state.  Errors: WICI_E_ARG (NULL or identical
+ * models, a differing configuration, NULL/small/misaligned regions),
+ * WICI_E_STATE (m already bound, src without complete weights). */
+wici_status wici_bind_memory_shared(wici_model* m, const wici_model* src, void* d_kv,
+                                    size_t kv_bytes, void* d_scratch, size_t scratch_bytes);
+
+/* One greedy decode step for n clients at once: models[0..n) must share one
+ * weight copy (wici_bind_memory_shared) and configuration (also kv_dtype and
+ * kv_page), be distinct, prefilled and below capacity.  The weights are read
+ * once for all n sequences: row b of every activation matrix is sequence b, the
+ * projections run as matrix products (on the matrix cores in models[0]'s
+ * prefill mode), and each sequence's RoPE, KV append, attention and argmax use
+ * its own cache and position.  tokens_in (host, n entries, or NULL for all -1)
+ * as token_in of wici_decode_step; next_tokens (host, n) receives each next
+ * token; logits (host, n * vocab, may be NULL) each sequence's fp32 logits,
+ * row b for sequence b.  Runs on models[0]'s stream and scratch (n <= its prefill_chunk and
+ * <= 256).  Synchronous.  Errors: WICI_E_ARG (bad pointers or counts, models
+ * that do not share weights and configuration, duplicates, a token id >= vocab,
+ * n beyond the scratch), WICI_E_STATE (a model not ready, not prefilled or
+ * without a token to feed), WICI_E_CAPACITY (a model at max_seq),
+ * WICI_E_NUMERIC (a sequence's logits were not finite: its next token is -1,
+ * the other sequences advanced normally).  Errors are reported on models[0]. */
+wici_status wici_decode_batch(wici_model* const* models, int32_t n, const int32_t* tokens_in,
+                              int32_t* next_tokens, float* logits);
+
 /* Forget the sequence: position 0, KV pages returned to the pool.  Weights stay. */
 wici_status wici_reset_kv(wici_model* m);
 

@@ -29,7 +29,8 @@ WICI_FLAG_NO_GRAPH = 1
 EXPORTED = ["wici_create", "wici_memory_requirements", "wici_bind_memory", "wici_load_weights",
             "wici_prefill", "wici_decode_step", "wici_decode_n", "wici_reset_kv", "wici_position",
             "wici_read_kv", "wici_profile_decode_step", "wici_quantize_q8", "wici_md5",
-            "wici_load_weights_cached", "wici_last_error", "wici_destroy"]
+            "wici_load_weights_cached", "wici_bind_memory_shared", "wici_decode_batch",
+            "wici_last_error", "wici_destroy"]
 
 
 class WiciConfig(ctypes.Structure):
@@ -88,6 +89,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
         "wici_md5": ([P, sz, P], ctypes.c_int),
         "wici_load_weights_cached": ([P, ctypes.POINTER(WiciTensor), P, i32, ctypes.c_char_p,
                                       ctypes.c_int64, P], ctypes.c_int),
+        "wici_bind_memory_shared": ([P, P, P, sz, P, sz], ctypes.c_int),
+        "wici_decode_batch": ([P, i32, P, P, P], ctypes.c_int),
         "wici_last_error": ([P], ctypes.c_char_p),
         "wici_destroy": ([P], None),
     }
@@ -205,7 +208,10 @@ class WiciModel:
 
     def __init__(self, cfg: ModelConfig, *, prefill_mode: str | None = None, graph: bool = True,
                  max_seq: int | None = None, prefill_chunk: int | None = None,
-                 kv_page: int | None = None, device: int = 0):
+                 kv_page: int | None = None, device: int = 0,
+                 share_weights_of: "WiciModel | None" = None):
+        """share_weights_of: another (loaded) model whose weights this one uses
+        (wici_bind_memory_shared); only the KV cache and scratch are allocated."""
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("WiciModel needs a HIP GPU")
@@ -216,7 +222,9 @@ class WiciModel:
         wb, kb, sb = memory_requirements(self.c)
         self.mem_bytes = (wb, kb, sb)
         self.stream = torch.cuda.Stream(self.device)
-        self._w = torch.empty(wb, dtype=torch.uint8, device=self.device)
+        self._src = share_weights_of
+        self._w = None if share_weights_of is not None else \
+            torch.empty(wb, dtype=torch.uint8, device=self.device)
         self._kv = torch.empty(kb, dtype=torch.uint8, device=self.device)
         self._s = torch.empty(sb, dtype=torch.uint8, device=self.device)
         torch.cuda.synchronize(self.device)
@@ -224,8 +232,14 @@ class WiciModel:
         self._check(self.lib.wici_create(ctypes.byref(self.c), ctypes.c_void_p(self.stream.cuda_stream),
                                          ctypes.byref(h)), "wici_create", handle=None)
         self.h = h
-        self._check(self.lib.wici_bind_memory(self.h, self._w.data_ptr(), wb, self._kv.data_ptr(), kb,
-                                              self._s.data_ptr(), sb), "wici_bind_memory")
+        if share_weights_of is not None:
+            self._check(self.lib.wici_bind_memory_shared(self.h, share_weights_of.h,
+                                                         self._kv.data_ptr(), kb,
+                                                         self._s.data_ptr(), sb),
+                        "wici_bind_memory_shared")
+        else:
+            self._check(self.lib.wici_bind_memory(self.h, self._w.data_ptr(), wb, self._kv.data_ptr(),
+                                                  kb, self._s.data_ptr(), sb), "wici_bind_memory")
         self._logits = np.empty(cfg.vocab, np.float32)
 
     def _check(self, st: int, what: str, handle="self"):
@@ -344,6 +358,25 @@ class WiciModel:
             ids.append(tok)
             logs.append(lg)
         return ids, logs
+
+    @staticmethod
+    def decode_batch(models, tokens_in=None, want_logits: bool = False):
+        """One greedy step for several models sharing weights (wici_decode_batch);
+        returns the next token of each (and their logits [n, vocab] if asked)."""
+        n = len(models)
+        arr = (ctypes.c_void_p * n)(*[m.h.value if isinstance(m.h, ctypes.c_void_p) else m.h
+                                      for m in models])
+        toks = None
+        if tokens_in is not None:
+            toks = np.ascontiguousarray(np.asarray(tokens_in, np.int32))
+        out = np.zeros(n, np.int32)
+        lg = np.empty((n, models[0].cfg.vocab), np.float32) if want_logits else None
+        lead = models[0]
+        lead._check(lead.lib.wici_decode_batch(arr, n, toks.ctypes.data if toks is not None else None,
+                                               out.ctypes.data,
+                                               lg.ctypes.data if lg is not None else None),
+                    "wici_decode_batch")
+        return (out, lg) if want_logits else out
 
     def close(self) -> None:
         if getattr(self, "h", None):

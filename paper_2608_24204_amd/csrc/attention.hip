@@ -39,12 +39,28 @@ __device__ __forceinline__ size_t kv_off(const KvLayout& kv, int pos, int which,
 constexpr int kChunk = 64;       // positions per decode split
 constexpr int kMaxSplits = 256;  // splits the merge kernel holds in LDS
 
+// With seqs != nullptr the launch is batched: blockIdx.z is the sequence, whose
+// KV pool, page table and position come from seqs[z] (layer `layer`), whose
+// queries start at q_in + z * q_stride and whose partials follow the previous
+// sequence's.
 template <int HD, typename KT, int G>
 __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q_in,
                                                      KvLayout kv,
                                                      const DecodeState* __restrict__ st,
                                                      float* __restrict__ part_o,
-                                                     float* __restrict__ part_ml) {
+                                                     float* __restrict__ part_ml,
+                                                     const SeqDesc* __restrict__ seqs, int layer,
+                                                     int q_stride) {
+  if (seqs) {
+    const SeqDesc sd = seqs[blockIdx.z];
+    kv.base = static_cast<char*>(sd.kv) + (size_t)layer * sd.kv_layer_stride;
+    kv.table = sd.table;
+    st = static_cast<const DecodeState*>(sd.state);
+    q_in += (size_t)blockIdx.z * q_stride;
+    const size_t heads = (size_t)kv.n_kv * G * gridDim.x;
+    part_o += (size_t)blockIdx.z * heads * HD;
+    part_ml += (size_t)blockIdx.z * heads * 2;
+  }
   constexpr int LPP = HD / 8;       // lanes per position (8 elements each)
   constexpr int PPW = 64 / LPP;     // positions per wave per pass
   constexpr int PPB = 4 * PPW;      // positions per block per pass
@@ -237,13 +253,67 @@ __global__ __launch_bounds__(HD) void k_attn_merge(const float* __restrict__ par
   out[(size_t)h * HD + d] = o / L;
 }
 
+// Batched merge: block (h, b) merges head h of sequence b into the activation
+// buffer of the O projection (row b).
+template <int HD>
+__global__ __launch_bounds__(HD) void k_attn_merge_batch(const float* __restrict__ part_o,
+                                                         const float* __restrict__ part_ml,
+                                                         int nsplit,
+                                                         const SeqDesc* __restrict__ seqs,
+                                                         ActBuf out) {
+  __shared__ float w[kMaxSplits];
+  __shared__ float red[HD / 64];
+  const int h = blockIdx.x, b = blockIdx.y, Hq = gridDim.x;
+  const int d = threadIdx.x, lane = d & 63, wv = d >> 6;
+  const int pos = static_cast<const DecodeState*>(seqs[b].state)->pos;
+  const int active = (pos + kChunk) / kChunk;
+  const size_t head = (size_t)b * Hq + h;
+  const float* ml = part_ml + head * nsplit * 2;
+  float mloc = -INFINITY;
+  for (int s = d; s < active; s += HD) mloc = fmaxf(mloc, ml[2 * s]);
+  mloc = wave_max(mloc);
+  if (lane == 0) red[wv] = mloc;
+  __syncthreads();
+  float M = red[0];
+#pragma unroll
+  for (int i = 1; i < HD / 64; ++i) M = fmaxf(M, red[i]);
+  float lsum = 0.f;
+  for (int s = d; s < active; s += HD) {
+    const float e = __expf(ml[2 * s] - M);
+    w[s] = e;
+    lsum += e * ml[2 * s + 1];
+  }
+  lsum = wave_sum(lsum);
+  __syncthreads();
+  if (lane == 0) red[wv] = lsum;
+  __syncthreads();
+  float L = 0.f;
+#pragma unroll
+  for (int i = 0; i < HD / 64; ++i) L += red[i];
+  const float* po = part_o + head * nsplit * HD + d;
+  float o = 0.f;
+  for (int s = 0; s < active; ++s) o += w[s] * po[(size_t)s * HD];
+  store_act(out, ((size_t)b * Hq + h) * HD + d, o / L);
+}
+
 template <int HD, typename KT, int G>
 static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const DecodeState* st,
                                 int nsplit, float* part_o, float* part_ml, float* out,
                                 hipStream_t s) {
   launch_k(k_attn_decode<HD, KT, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv, st,
-           part_o, part_ml);
+           part_o, part_ml, (const SeqDesc*)nullptr, 0, 0);
   launch_k(k_attn_merge<HD>, dim3(Hq), dim3(HD), 0, s, kLast, part_o, part_ml, nsplit, st, out);
+  return hipGetLastError();
+}
+
+template <int HD, typename KT, int G>
+static hipError_t attn_decode_batch_t(const float* q, int q_stride, int B, int Hq, KvLayout kv,
+                                      const SeqDesc* seqs, int layer, int nsplit, float* part_o,
+                                      float* part_ml, const ActBuf& out, hipStream_t s) {
+  hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv, B), dim3(256), 0, s, q,
+                     kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer, q_stride);
+  hipLaunchKernelGGL((k_attn_merge_batch<HD>), dim3(Hq, B), dim3(HD), 0, s, part_o, part_ml,
+                     nsplit, seqs, out);
   return hipGetLastError();
 }
 
@@ -259,6 +329,39 @@ static hipError_t attn_decode_g(int G, const float* q, int Hq, KvLayout kv,
     case 8: return attn_decode_t<HD, KT, 8>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+template <int HD, typename KT>
+static hipError_t attn_decode_batch_g(int G, const float* q, int q_stride, int B, int Hq,
+                                      KvLayout kv, const SeqDesc* seqs, int layer, int nsplit,
+                                      float* part_o, float* part_ml, const ActBuf& out,
+                                      hipStream_t s) {
+#define WICI_B(GG) \
+  case GG: return attn_decode_batch_t<HD, KT, GG>(q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s)
+  switch (G) {
+    WICI_B(1); WICI_B(2); WICI_B(4); WICI_B(5); WICI_B(8);
+    default: return hipErrorInvalidValue;
+  }
+#undef WICI_B
+}
+
+hipError_t launch_attn_decode_batch(bool kv_bf16, const float* q, int q_stride, int B, int Hq,
+                                    KvLayout kv, const SeqDesc* seqs, int layer, int nsplit,
+                                    float* part_o, float* part_ml, const ActBuf& out,
+                                    hipStream_t s) {
+  if (B < 1 || nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos || kv.n_kv < 1 ||
+      Hq % kv.n_kv)
+    return hipErrorInvalidValue;
+  const int G = Hq / kv.n_kv;
+  if (kv.hd == 128) {
+    if (kv_bf16) return attn_decode_batch_g<128, bf16_t>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s);
+    return attn_decode_batch_g<128, float>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s);
+  }
+  if (kv.hd == 64) {
+    if (kv_bf16) return attn_decode_batch_g<64, bf16_t>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s);
+    return attn_decode_batch_g<64, float>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 int attn_decode_splits(int max_seq) { return (max_seq + kChunk - 1) / kChunk; }

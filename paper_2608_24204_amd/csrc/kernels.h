@@ -92,6 +92,34 @@ hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int
                                const ActBuf& y, hipStream_t st);
 
 
+// One sequence of a batched decode step (a device array of B of them).
+struct SeqDesc {
+  void* kv;                  // the sequence's KV pool (layer 0; layer l at + l * kv_layer_stride)
+  size_t kv_layer_stride;    // bytes per layer
+  const int32_t* table;      // its page table
+  void* state;               // its DecodeState
+  int32_t* hist;             // its token history [max_seq]
+};
+
+// Batched decode helpers (row b = sequence b).
+hipError_t launch_gather_tokens(const SeqDesc* seqs, int B, int32_t* tokens, hipStream_t st);
+// Rotate row b's queries in place (times q_scale) and keys at sequence b's position,
+// append keys and values to its cache (layer `layer`; kv gives page, heads, hd).
+hipError_t launch_rope_append_batch(bool kv_bf16, float* qkv, int B, int Hq, const float* cos_t,
+                                    const float* sin_t, const SeqDesc* seqs, int layer,
+                                    KvLayout kv, float q_scale, hipStream_t st);
+// Greedy token per row of logits [B, V]; advances each sequence's state and history
+// (a row with a non-finite logit gets token -1 and the failed flag).
+hipError_t launch_argmax_rows(const float* logits, int B, int V, const SeqDesc* seqs,
+                              hipStream_t st);
+// Batched decode attention: row b's queries (q + b * q_stride, rotated and scaled)
+// over sequence b's cache [0, pos_b]; partials [B][Hq][nsplit]; out is the
+// activation buffer of the O projection, row b at b * Hq * hd.
+hipError_t launch_attn_decode_batch(bool kv_bf16, const float* q, int q_stride, int B, int Hq,
+                                    KvLayout kv, const SeqDesc* seqs, int layer, int nsplit,
+                                    float* part_o, float* part_ml, const ActBuf& out,
+                                    hipStream_t st);
+
 // Prefill: rotate q (in place) and k of T rows at positions p0..p0+T-1 and
 // append k, v to the cache.  qkv rows are [Hq*hd | Hkv*hd | Hkv*hd] fp32.
 hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <string>
 #include <unordered_map>
@@ -26,6 +27,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kMaxGemvBlocks = 1024;
+constexpr int kMaxBatch = 256;  // sequences per batched decode step
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 size_t dsize(int32_t dt) { return dt == WICI_BF16 ? 2 : 4; }
@@ -38,7 +40,7 @@ struct Layout {
   int n_pages;
   size_t kv_layer_stride, kv_bytes;
   // scratch
-  size_t x, a, qkv, att, h, logits, parts, part_o, part_ml, tokens, table, state, hist;
+  size_t x, a, qkv, att, h, logits, parts, part_o, part_ml, tokens, table, state, hist, seqs;
   size_t scratch_bytes;
   int nsplit;
 };
@@ -128,6 +130,7 @@ Layout make_layout(const wici_config& c) {
   L.table = o; o = align_up(o + (size_t)L.n_pages * 4);
   L.state = o; o = align_up(o + sizeof(DecodeState));
   L.hist = o; o = align_up(o + (size_t)c.max_seq * 4);  // token emitted after each position
+  L.seqs = o; o = align_up(o + (size_t)kMaxBatch * sizeof(wici::SeqDesc));  // batched decode
   L.scratch_bytes = o;
   return L;
 }
@@ -160,6 +163,7 @@ struct wici_model {
   int n_loaded = 0;
   int32_t pos = 0;
   bool have_token = false;
+  bool shared_weights = false;  // weights bound from another model (read-only here)
   DecodeState* h_state = nullptr;  // pinned staging
   hipGraph_t graph = nullptr;
   hipGraphExec_t gexec = nullptr;
@@ -360,6 +364,86 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   return hipSuccess;
 }
 
+// Enqueue one batched decode step of B sequences (descriptors already in the
+// lead model's scratch) on the lead's stream, in its scratch: row b of every
+// activation matrix is sequence b.  The projections are the prefill products
+// (matrix cores with the lead's prefill mode, or the vector product), the
+// per-sequence parts (RoPE and append, attention, argmax) read the descriptors.
+hipError_t enqueue_decode_batch(wici_model* m, int B) {
+  const wici_config& c = m->cfg;
+  const Layout& L = m->L;
+  const int wb = c.weight_dtype;
+  const bool kb = c.kv_dtype == WICI_BF16;
+  const int d = c.d_model, F = c.ffn_dim, qd = c.n_heads * c.head_dim;
+  const int nqkv = qd + 2 * c.n_kv_heads * c.head_dim;
+  const size_t C = c.prefill_chunk;
+  const int nt = c.prefill_mode == WICI_PREFILL_F32 ? 0
+                 : c.prefill_mode == WICI_PREFILL_BF16 ? 1
+                 : c.prefill_mode == WICI_PREFILL_BF16X2 ? 2 : 3;
+  auto act = [&](size_t off, size_t width) {
+    wici::ActBuf b;
+    b.f32 = m->S<float>(off);
+    b.planes = m->S<wici::bf16_t>(off);
+    b.plane_stride = C * width;
+    b.nt = nt;
+    return b;
+  };
+  const wici::ActBuf a = act(L.a, d), att = act(L.att, qd), h = act(L.h, F);
+  const wici::ActBuf none{};
+  const wici::SeqDesc* seqs = m->S<wici::SeqDesc>(L.seqs);
+  float* x = m->S<float>(L.x);
+  float* qkv = m->S<float>(L.qkv);
+  // attention partials and the logits live in the FFN buffer, free at those times
+  float* part_o = m->S<float>(L.h);
+  float* part_ml = part_o + (size_t)B * c.n_heads * L.nsplit * c.head_dim;
+  float* logits = m->S<float>(L.h);
+  wici::KvLayout kv = m->kv(0);  // geometry; pool and table come per sequence
+  const float q_scale = 1.0f / std::sqrt((float)c.head_dim);
+  hipStream_t s = m->stream;
+  hipError_t e;
+#define WICI_TRY(call) \
+  do {                 \
+    if ((e = (call))) return e; \
+  } while (0)
+  WICI_TRY(wici::launch_gather_tokens(seqs, B, m->S<int32_t>(L.tokens), s));
+  WICI_TRY(wici::launch_embed(wb, m->dw + L.embed, c.vocab, d, m->S<int32_t>(L.tokens), B,
+                              nullptr, x, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, B, d,
+                                       a, s));
+    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_STORE, a, d, m->dw + m->layer(l, L.l_wqkv), B,
+                               nqkv, d, qkv, nqkv, none, 0, s));
+    WICI_TRY(wici::launch_rope_append_batch(kb, qkv, B, c.n_heads, m->W<float>(L.rope_cos),
+                                            m->W<float>(L.rope_sin), seqs, l, kv, q_scale, s));
+    WICI_TRY(wici::launch_attn_decode_batch(kb, qkv, nqkv, B, c.n_heads, kv, seqs, l, L.nsplit,
+                                            part_o, part_ml, att, s));
+    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_RESID, att, qd, m->dw + m->layer(l, L.l_wo), B, d,
+                               qd, x, d, none, 0, s));
+    WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_fnorm)), c.rms_eps, B, d,
+                                       a, s));
+    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_SWIGLU, a, d, m->dw + m->layer(l, L.l_wgu), B,
+                               2 * F, d, nullptr, 0, h, F, s));
+    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_RESID, h, F, m->dw + m->layer(l, L.l_wdown), B, d,
+                               F, x, d, none, 0, s));
+  }
+  WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(L.final_norm), c.rms_eps, B, d, a, s));
+  WICI_TRY(wici::launch_gemm(wb, wici::GEMV_STORE, a, d, m->dw + L.lm_head, B, c.vocab, d, logits,
+                             c.vocab, none, 0, s));
+  WICI_TRY(wici::launch_argmax_rows(logits, B, c.vocab, seqs, s));
+#undef WICI_TRY
+  return hipSuccess;
+}
+
+// Configurations whose weight regions are interchangeable (shapes, storage,
+// norm eps, RoPE tables, capacity).
+bool same_weights_geometry(const wici_config& a, const wici_config& b) {
+  return a.n_layers == b.n_layers && a.d_model == b.d_model && a.n_heads == b.n_heads &&
+         a.n_kv_heads == b.n_kv_heads && a.head_dim == b.head_dim && a.ffn_dim == b.ffn_dim &&
+         a.vocab == b.vocab && a.rms_eps == b.rms_eps && a.rope_base == b.rope_base &&
+         a.tied_embeddings == b.tied_embeddings && a.weight_dtype == b.weight_dtype &&
+         a.max_seq == b.max_seq;
+}
+
 wici_status finish_step(wici_model* m, int32_t* tok, float* logits) {
   HIP_TRY(m, hipMemcpyAsync(m->h_state, m->ds + m->L.state, sizeof(DecodeState),
                             hipMemcpyDeviceToHost, m->stream));
@@ -476,6 +560,8 @@ wici_status wici_load_weights(wici_model* m, const wici_tensor* tensors, int32_t
   if (!m) return WICI_E_ARG;
   if (m->failed) return WICI_E_STATE;
   if (!m->bound) return fail(m, WICI_E_STATE, "wici_bind_memory must come first");
+  if (m->shared_weights)
+    return fail(m, WICI_E_STATE, "weights are shared with another model (load them there)");
   if (n_tensors < 0 || (n_tensors > 0 && !tensors)) return fail(m, WICI_E_ARG, "bad tensor list");
   std::vector<int> idx(n_tensors);
   std::vector<uint8_t> seen(m->specs.size(), 0);
@@ -721,6 +807,99 @@ wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* n
   HIP_TRY(m, e3);
   *n_written = n;
   return finish_step(m, next_token, nullptr);
+}
+
+wici_status wici_bind_memory_shared(wici_model* m, const wici_model* src, void* d_kv,
+                                    size_t kv_bytes, void* d_scratch, size_t scratch_bytes) {
+  if (!m || !src || m == src) return WICI_E_ARG;
+  if (m->failed) return WICI_E_STATE;
+  if (m->bound) return fail(m, WICI_E_STATE, "memory already bound");
+  if (src->failed || !src->ready())
+    return fail(m, WICI_E_STATE, "the source model has no complete weights");
+  if (!same_weights_geometry(m->cfg, src->cfg))
+    return fail(m, WICI_E_ARG, "configuration differs from the source model's weights");
+  if (!d_kv || !d_scratch) return fail(m, WICI_E_ARG, "NULL device pointer");
+  if (kv_bytes < m->L.kv_bytes || scratch_bytes < m->L.scratch_bytes)
+    return fail(m, WICI_E_ARG, "device region too small");
+  if (((uintptr_t)d_kv | (uintptr_t)d_scratch) % kAlign)
+    return fail(m, WICI_E_ARG, "device regions must be 256-byte aligned");
+  m->dw = src->dw;
+  m->dkv = static_cast<char*>(d_kv);
+  m->ds = static_cast<char*>(d_scratch);
+  HIP_TRY(m, hipHostMalloc((void**)&m->h_state, sizeof(DecodeState), hipHostMallocDefault));
+  HIP_TRY(m, wici::launch_init_block_table(m->S<int32_t>(m->L.table), m->L.n_pages, m->stream));
+  HIP_TRY(m, wici::launch_reset_state(m->ds + m->L.state, m->stream));
+  HIP_TRY(m, hipStreamSynchronize(m->stream));
+  m->loaded.assign(m->specs.size(), 1);
+  m->n_loaded = (int)m->specs.size();
+  m->shared_weights = true;
+  m->bound = true;
+  m->pos = 0;
+  m->have_token = false;
+  return WICI_OK;
+}
+
+wici_status wici_decode_batch(wici_model* const* models, int32_t n, const int32_t* tokens_in,
+                              int32_t* next_tokens, float* logits) {
+  if (!models || n < 1 || !next_tokens) return WICI_E_ARG;
+  wici_model* lead = models[0];
+  if (!lead) return WICI_E_ARG;
+  if (lead->failed) return WICI_E_STATE;
+  if (n > kMaxBatch || n > lead->cfg.prefill_chunk)
+    return fail(lead, WICI_E_ARG, "%d sequences: at most %d (and the prefill chunk)", n,
+                kMaxBatch);
+  const wici_config& c = lead->cfg;
+  const Layout& L = lead->L;
+  // the FFN buffer holds the attention partials and the logits of all sequences
+  const size_t h_bytes = (size_t)c.prefill_chunk * c.ffn_dim * 6;
+  const size_t need = std::max((size_t)n * c.n_heads * L.nsplit * (c.head_dim + 2) * 4,
+                               (size_t)n * c.vocab * 4);
+  if (need > h_bytes) return fail(lead, WICI_E_ARG, "%d sequences exceed the batch scratch", n);
+  std::vector<wici::SeqDesc> sd(n);
+  for (int b = 0; b < n; ++b) {
+    wici_model* mb = models[b];
+    if (!mb) return fail(lead, WICI_E_ARG, "NULL model %d", b);
+    for (int j = 0; j < b; ++j)
+      if (models[j] == mb) return fail(lead, WICI_E_ARG, "model %d appears twice", b);
+    if (mb->failed || !mb->ready()) return fail(lead, WICI_E_STATE, "model %d not ready", b);
+    if (mb->dw != lead->dw || !same_weights_geometry(mb->cfg, c) ||
+        mb->cfg.kv_dtype != c.kv_dtype || mb->cfg.kv_page != c.kv_page)
+      return fail(lead, WICI_E_ARG, "model %d does not share the lead's weights and config", b);
+    const int32_t t = tokens_in ? tokens_in[b] : -1;
+    if (t >= c.vocab) return fail(lead, WICI_E_ARG, "token id %d >= vocab", t);
+    if (mb->pos < 1) return fail(lead, WICI_E_STATE, "model %d: decode before prefill", b);
+    if (t < 0 && !mb->have_token) return fail(lead, WICI_E_STATE, "model %d: no token", b);
+    if (mb->pos + 1 > c.max_seq) return fail(lead, WICI_E_CAPACITY, "model %d is full", b);
+    sd[b].kv = mb->dkv;
+    sd[b].kv_layer_stride = mb->L.kv_layer_stride;
+    sd[b].table = mb->S<int32_t>(mb->L.table);
+    sd[b].state = mb->ds + mb->L.state;
+    sd[b].hist = mb->S<int32_t>(mb->L.hist);
+  }
+  for (int b = 0; b < n; ++b)
+    if (tokens_in && tokens_in[b] >= 0)
+      HIP_TRY(lead, wici::launch_set_token(models[b]->ds + models[b]->L.state, tokens_in[b],
+                                           lead->stream));
+  HIP_TRY(lead, hipMemcpyAsync(lead->ds + L.seqs, sd.data(), n * sizeof(wici::SeqDesc),
+                               hipMemcpyHostToDevice, lead->stream));
+  HIP_TRY(lead, enqueue_decode_batch(lead, n));
+  std::vector<DecodeState> st(n);
+  for (int b = 0; b < n; ++b)
+    HIP_TRY(lead, hipMemcpyAsync(&st[b], models[b]->ds + models[b]->L.state, sizeof(DecodeState),
+                                 hipMemcpyDeviceToHost, lead->stream));
+  if (logits)
+    HIP_TRY(lead, hipMemcpyAsync(logits, lead->ds + L.h, (size_t)n * c.vocab * 4,
+                                 hipMemcpyDeviceToHost, lead->stream));
+  HIP_TRY(lead, hipStreamSynchronize(lead->stream));
+  int bad = -1;
+  for (int b = 0; b < n; ++b) {
+    models[b]->pos = st[b].pos;
+    models[b]->have_token = !st[b].bad;
+    next_tokens[b] = st[b].bad ? -1 : st[b].token;
+    if (st[b].bad && bad < 0) bad = b;
+  }
+  if (bad >= 0) return fail(lead, WICI_E_NUMERIC, "non-finite logits in sequence %d", bad);
+  return WICI_OK;
 }
 
 wici_status wici_reset_kv(wici_model* m) {
