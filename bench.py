@@ -186,6 +186,45 @@ def model_cache_sweep(cfg_name, store_root, thresholds_mib):
     return 0
 
 
+def batch_sweep(cfg_name, batches, n_steps):
+    """Aggregate decode tokens/s of B clients sharing one weight copy, advanced
+    together by wici_decode_batch (each prefilled with its own prompt of the
+    workload's length).  Prints one JSON line."""
+    import torch
+
+    from paper_2608_24204_amd import binding, configs, inputs
+    cfg = configs.CONFIGS[cfg_name]
+    w = inputs.make_weights(cfg)
+    rng = np.random.default_rng(123)
+    top = max(batches)
+    lead = binding.WiciModel(cfg)
+    lead.load_weights(w)
+    ms = [lead] + [binding.WiciModel(cfg, share_weights_of=lead) for _ in range(top - 1)]
+    rows = []
+    for B in batches:
+        group = ms[:B]
+        for m in group:
+            m.reset_kv()
+            m.prefill(rng.integers(0, cfg.vocab, cfg.prompt_len).astype(np.int32))
+        lead.decode_batch(group)                       # warm-up step
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n_steps):
+            lead.decode_batch(group)
+        dt = time.perf_counter() - t0
+        ctx = cfg.prompt_len + 1 + n_steps / 2
+        kv = B * ctx * cfg.n_layers * 2 * cfg.kv_dim * cfg.kvbytes
+        wbytes = cfg.decode_bytes_per_token(0)
+        rows.append({"batch": B, "tok_s": B * n_steps / dt, "step_ms": dt / n_steps * 1e3,
+                     "hbm_frac": (wbytes + kv) * n_steps / dt / HBM_PEAK})
+        log(f"batch {B}: {B * n_steps / dt:.1f} tok/s, {dt / n_steps * 1e3:.2f} ms/step")
+    for m in ms:
+        m.close()
+    print(json.dumps({"metric": "batched decode tokens/s (clients sharing weights)",
+                      "config": cfg_name, "steps": n_steps, "rows": rows}), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -205,7 +244,12 @@ def main(argv=None):
                     help="instead of the benchmark: model load time against the caching "
                          "threshold (store under --store-root)")
     ap.add_argument("--store-root", default=os.environ.get("TMPDIR", "/tmp"))
+    ap.add_argument("--batch-sweep", default=None, metavar="B1,B2,...",
+                    help="instead of the benchmark: aggregate tokens/s of batched decode")
     args = ap.parse_args(argv)
+    if args.batch_sweep:
+        return batch_sweep(args.config, [int(b) for b in args.batch_sweep.split(",")],
+                           args.decode or 32)
     if args.model_cache:
         return model_cache_sweep(args.config, args.store_root,
                                  [0, 0.0625, 1, 16, 64, 256, 4096])

@@ -25,8 +25,9 @@
  *  - A model is not thread-safe; use one model per thread (one client per
  *    server thread, as in the paper's context management, Sec. "WiCi Library").
  *  - Device memory is owned by the caller (see wici_bind_memory); the library
- *    owns only host state, a captured decode graph and a 16-byte pinned host
- *    staging buffer, all released by wici_destroy.
+ *    owns only host state, captured decode graphs (the per-token step, and the
+ *    batched step per batch size it led) and a 16-byte pinned host staging
+ *    buffer, all released by wici_destroy.
  */
 #ifndef WICI_H
 #define WICI_H

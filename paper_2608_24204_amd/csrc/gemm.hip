@@ -228,6 +228,120 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
       }
 }
 
+// ------------------------------------------------------------ skinny (M <= 32)
+// For a handful of rows (a batched decode step: one row per sequence) the product
+// is bound by streaming W, like the decode GEMV, not by the matrix cores.  A
+// workgroup owns 16 TN columns (weight rows) and all M (<= 16 TM) rows; its four
+// wavefronts split K and add their partial tiles through LDS at the end.  A
+// wavefront loads its weight fragments straight from memory into the operand
+// registers of v_mfma_f32_16x16x32_bf16 (lane l: row n0 + 16 j + l % 16, eight
+// consecutive K at 8 (l / 16)), two K steps per batch, double-buffered, every
+// load unconditional (rows clamped; rows of A past M are clamped too and their
+// outputs dropped), so a batch's wait leaves the next batch in flight.  The
+// activation fragments (NT bf16 planes, TM row tiles) come from L2.
+template <int NT, int TM, int TN>
+struct SkinnyBatch {
+  static constexpr int D = 2;  // K steps per batch
+  bf16x8_t w[D][TN];
+  bf16x8_t a[D][NT][TM];
+};
+
+template <int NT, int TM, int TN, int EPI>
+__global__ __launch_bounds__(256) void k_gemm_skinny(const bf16_t* __restrict__ A,
+                                                     size_t a_plane, int lda,
+                                                     const bf16_t* __restrict__ W, int M, int N,
+                                                     int K, float* __restrict__ C, int ldc,
+                                                     ActBuf H, int ldh) {
+  using Bt = SkinnyBatch<NT, TM, TN>;
+  constexpr int D = Bt::D;
+  __shared__ floatx4_t red[4][TM][TN][64];
+  const int n0 = blockIdx.x * 16 * TN;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int fr = lane & 15, fk = (lane >> 4) * 8;
+  const int KT = K / kBK;
+  const int kt0 = wave * KT / 4, kt1 = (wave + 1) * KT / 4, nst = kt1 - kt0;
+  const int nb = (nst + D - 1) / D;  // batches of this wavefront
+  const bf16_t* wrow[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) wrow[j] = W + (size_t)min(n0 + j * 16 + fr, N - 1) * K + fk;
+  const bf16_t* arow[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) arow[i] = A + (size_t)min(i * 16 + fr, M - 1) * lda + fk;
+
+  auto issue = [&](Bt& buf, int b) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int k = min(kt0 + b * D + d, KT - 1) * kBK;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        buf.w[d][j] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(wrow[j] + k));
+#pragma unroll
+      for (int p = 0; p < NT; ++p)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          buf.a[d][p][i] = *reinterpret_cast<const bf16x8_t*>(arow[i] + p * a_plane + k);
+    }
+  };
+  floatx4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const Bt& buf, int b) {
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+      if (b * D + d < nst) {
+#pragma unroll
+        for (int p = 0; p < NT; ++p)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(buf.a[d][p][i], buf.w[d][j],
+                                                                  acc[i][j], 0, 0, 0);
+      }
+  };
+  Bt b0, b1;
+  issue(b0, 0);
+  int b = 0;
+  for (; b + 2 < nb; b += 2) {
+    issue(b1, b + 1);
+    compute(b0, b);
+    issue(b0, b + 2);
+    compute(b1, b + 1);
+  }
+  if (b + 1 < nb) {
+    issue(b1, b + 1);
+    compute(b0, b);
+    compute(b1, b + 1);
+  } else if (b < nb) {
+    compute(b0, b);
+  }
+
+  // sum the four K ranges, then the epilogue (lane: rows 16 i + 4 (l / 16) + r,
+  // column l % 16 of tile j)
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) red[wave][i][j][lane] = acc[i][j];
+  __syncthreads();
+  for (int t = wave; t < TM * TN; t += 4) {
+    const int i = t / TN, j = t % TN;
+    floatx4_t v = red[0][i][j][lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const floatx4_t u = red[w][i][j][lane];
+      v[0] += u[0]; v[1] += u[1]; v[2] += u[2]; v[3] += u[3];
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = i * 16 + (lane >> 4) * 4 + r, n = n0 + j * 16 + (lane & 15);
+      const float o = EPI == GEMV_SWIGLU ? __shfl_xor(v[r], 1) : 0.f;
+      epi_out<EPI>(C, ldc, H, ldh, M, N, m, n, v[r], o);
+    }
+  }
+}
+
 // ------------------------------------------------------------------- vector fp32
 template <typename WT, int EPI>
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, int lda,
@@ -320,6 +434,41 @@ static hipError_t gemm_mfma(const ActBuf& A, int lda, const void* W, int M, int 
   }
 }
 
+template <int NT, int TM, int TN, int EPI>
+static hipError_t gemm_skinny_launch(const ActBuf& A, int lda, const void* W, int M, int N, int K,
+                                     float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
+  const int grid = (N + 16 * TN - 1) / (16 * TN);
+  hipLaunchKernelGGL((k_gemm_skinny<NT, TM, TN, EPI>), dim3(grid), dim3(256), 0, st, A.planes,
+                     A.plane_stride, lda, static_cast<const bf16_t*>(W), M, N, K, C, ldc, H, ldh);
+  return hipGetLastError();
+}
+
+// Columns per workgroup: as many as still leave >= 512 workgroups (2 per CU).
+template <int NT, int TM, int EPI>
+static hipError_t gemm_skinny_tn(const ActBuf& A, int lda, const void* W, int M, int N, int K,
+                                 float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
+  if (N >= 64 * 512)
+    return gemm_skinny_launch<NT, TM, 4, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+  if (N >= 32 * 512)
+    return gemm_skinny_launch<NT, TM, 2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+  return gemm_skinny_launch<NT, TM, 1, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+}
+
+template <int EPI>
+static hipError_t gemm_skinny(const ActBuf& A, int lda, const void* W, int M, int N, int K,
+                              float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
+#define WICI_SKT(NT_)                                                                         \
+  return M <= 16 ? gemm_skinny_tn<NT_, 1, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st)        \
+                 : gemm_skinny_tn<NT_, 2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st)
+  switch (A.nt) {
+    case 1: WICI_SKT(1);
+    case 2: WICI_SKT(2);
+    case 3: WICI_SKT(3);
+    default: return hipErrorInvalidValue;
+  }
+#undef WICI_SKT
+}
+
 template <typename WT, int EPI>
 static hipError_t gemm_f32(const ActBuf& A, int lda, const WT* W, int M, int N, int K, float* C,
                            int ldc, const ActBuf& H, int ldh, hipStream_t st) {
@@ -351,6 +500,9 @@ hipError_t launch_gemm(int wt, int epi, const ActBuf& A, int lda, const void* W,
 #undef WICI_F32
     return hipErrorInvalidValue;
   }
+#define WICI_SK(E) gemm_skinny<E>(A, lda, W, M, N, K, C, ldc, H, ldh, st)
+  if (wt == W_BF16 && M <= 32) { WICI_EPI(WICI_SK) }
+#undef WICI_SK
 #define WICI_MF(E) gemm_mfma<E, Q8_>(A, lda, W, M, N, K, C, ldc, H, ldh, st)
   if (wt == W_BF16) { constexpr bool Q8_ = false; WICI_EPI(WICI_MF) }
   if (wt == W_Q8) { constexpr bool Q8_ = true; WICI_EPI(WICI_MF) }

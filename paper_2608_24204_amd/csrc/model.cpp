@@ -167,6 +167,10 @@ struct wici_model {
   DecodeState* h_state = nullptr;  // pinned staging
   hipGraph_t graph = nullptr;
   hipGraphExec_t gexec = nullptr;
+  // batched decode steps led by this model, captured per batch size (the
+  // sequences' descriptors are read from device memory, so a graph serves any
+  // group of that size)
+  std::unordered_map<int, std::pair<hipGraph_t, hipGraphExec_t>> batch_graphs;
   int gemv_lm_blocks = 0;
 
   bool ready() const { return bound && n_loaded == (int)specs.size(); }
@@ -882,7 +886,27 @@ wici_status wici_decode_batch(wici_model* const* models, int32_t n, const int32_
                                            lead->stream));
   HIP_TRY(lead, hipMemcpyAsync(lead->ds + L.seqs, sd.data(), n * sizeof(wici::SeqDesc),
                                hipMemcpyHostToDevice, lead->stream));
-  HIP_TRY(lead, enqueue_decode_batch(lead, n));
+  const bool use_graph = lead->stream != nullptr && !(c.flags & WICI_FLAG_NO_GRAPH);
+  if (use_graph) {
+    auto it = lead->batch_graphs.find(n);
+    if (it == lead->batch_graphs.end()) {
+      HIP_TRY(lead, hipStreamBeginCapture(lead->stream, hipStreamCaptureModeThreadLocal));
+      const hipError_t e = enqueue_decode_batch(lead, n);
+      hipGraph_t g = nullptr;
+      const hipError_t e2 = hipStreamEndCapture(lead->stream, &g);
+      if (e != hipSuccess && g) (void)hipGraphDestroy(g);
+      HIP_TRY(lead, e);
+      HIP_TRY(lead, e2);
+      hipGraphExec_t ge = nullptr;
+      const hipError_t e3 = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+      if (e3 != hipSuccess) (void)hipGraphDestroy(g);
+      HIP_TRY(lead, e3);
+      it = lead->batch_graphs.emplace(n, std::make_pair(g, ge)).first;
+    }
+    HIP_TRY(lead, hipGraphLaunch(it->second.second, lead->stream));
+  } else {
+    HIP_TRY(lead, enqueue_decode_batch(lead, n));
+  }
   std::vector<DecodeState> st(n);
   for (int b = 0; b < n; ++b)
     HIP_TRY(lead, hipMemcpyAsync(&st[b], models[b]->ds + models[b]->L.state, sizeof(DecodeState),
@@ -954,6 +978,10 @@ void wici_destroy(wici_model* m) {
   if (!m) return;
   if (m->gexec) (void)hipGraphExecDestroy(m->gexec);
   if (m->graph) (void)hipGraphDestroy(m->graph);
+  for (auto& kv : m->batch_graphs) {
+    (void)hipGraphExecDestroy(kv.second.second);
+    (void)hipGraphDestroy(kv.second.first);
+  }
   if (m->h_state) (void)hipHostFree(m->h_state);
   delete m;
 }
