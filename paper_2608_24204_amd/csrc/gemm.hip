@@ -12,9 +12,10 @@
 //    wavefront a 64 x 64 sub-tile (4 x 4 matrix-core tiles, 64 accumulator
 //    registers);
 //  - both operands are staged through LDS in 32-deep K steps, double-buffered
-//    (rows padded to 80 B so the 16 rows a fragment read touches fall in distinct
-//    banks); the next step's global loads are in flight while the current
-//    step's matrix ops run, one barrier a step;
+//    (64-byte rows with the 16-byte chunks XOR-swizzled by row, so that neither
+//    the stores nor the fragment reads hit the same bank twice); the next
+//    step's global loads are in flight while the current step's matrix ops run,
+//    one barrier a step;
 //  - tiles are numbered A-tile-row-major and dealt to the 8 XCDs in contiguous
 //    ranges (workgroups are dispatched round-robin over XCDs), so the blocks
 //    resident on one XCD share an A row-tile through that XCD's L2.
@@ -39,7 +40,16 @@ __device__ __forceinline__ void epi_out(float* C, int ldc, const ActBuf& H, int 
 
 // --------------------------------------------------------------------- MFMA
 constexpr int kBK = 32;   // K per step (one v_mfma_f32_16x16x32_bf16 depth)
-constexpr int kLDK = 40;  // padded LDS row (bf16 elements)
+constexpr int kLDK = 32;  // LDS row (bf16 elements): 64 bytes, four 16-byte chunks
+
+// LDS position (bf16 elements) of 16-byte chunk `chunk` of tile row `row`: the chunk
+// index is XOR-ed with bits 2-3 of the row.  Sixteen lanes that store together
+// (4 consecutive rows x 4 chunks, as loaded from global memory) then cover four
+// disjoint 64-byte bank ranges, and sixteen lanes that read a fragment (16 rows,
+// one chunk) cover all 64 banks once: neither access conflicts.
+__device__ __forceinline__ int lds_chunk(int row, int chunk) {
+  return row * kLDK + 8 * (chunk ^ ((row >> 2) & 3));
+}
 
 // Q8 weights: a step of 32 along K is one quantisation block, so the codes go
 // through the matrix cores exactly (an integer in [-127, 127] is a bf16 value),
@@ -121,7 +131,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
       const int c = tid + i * NTH;
       if (c < A_CHUNKS) {
         const int p = c / (BM * 4), row = (c / 4) % BM, part = c % 4;
-        *reinterpret_cast<uint4*>(As + (((size_t)s * NT + p) * BM + row) * kLDK + part * 8) = ra[i];
+        *reinterpret_cast<uint4*>(As + ((size_t)s * NT + p) * BM * kLDK + lds_chunk(row, part)) = ra[i];
       }
     }
 #pragma unroll
@@ -140,11 +150,11 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
             const float hi = (float)((w >> (sh + 8)) & 0xffu) - 128.f;
             o[e] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xffff0000u);
           }
-          uint4* dst = reinterpret_cast<uint4*>(Bs + ((size_t)s * BN + row) * kLDK + part * 16);
-          dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
-          dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+          bf16_t* bt = Bs + (size_t)s * BN * kLDK;
+          *reinterpret_cast<uint4*>(bt + lds_chunk(row, 2 * part)) = make_uint4(o[0], o[1], o[2], o[3]);
+          *reinterpret_cast<uint4*>(bt + lds_chunk(row, 2 * part + 1)) = make_uint4(o[4], o[5], o[6], o[7]);
         } else {
-          *reinterpret_cast<uint4*>(Bs + ((size_t)s * BN + row) * kLDK + part * 8) = rw[i];
+          *reinterpret_cast<uint4*>(Bs + (size_t)s * BN * kLDK + lds_chunk(row, part)) = rw[i];
         }
       }
     }
@@ -171,7 +181,8 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
     bf16x8_t bfr[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + ((size_t)s * BN + wn * 64 + j * 16 + fr) * kLDK + fk);
+      bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + (size_t)s * BN * kLDK +
+                                                  lds_chunk(wn * 64 + j * 16 + fr, fk / 8));
     if constexpr (Q8) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -181,7 +192,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
 #pragma unroll
         for (int p = 0; p < NT; ++p) {
           const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(
-              As + (((size_t)s * NT + p) * BM + wm * 64 + i * 16 + fr) * kLDK + fk);
+              As + ((size_t)s * NT + p) * BM * kLDK + lds_chunk(wm * 64 + i * 16 + fr, fk / 8));
 #pragma unroll
           for (int j = 0; j < 4; ++j)
             part[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr[j], part[j], 0, 0, 0);
@@ -198,7 +209,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           af[i] = *reinterpret_cast<const bf16x8_t*>(
-              As + (((size_t)s * NT + p) * BM + wm * 64 + i * 16 + fr) * kLDK + fk);
+              As + ((size_t)s * NT + p) * BM * kLDK + lds_chunk(wm * 64 + i * 16 + fr, fk / 8));
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
