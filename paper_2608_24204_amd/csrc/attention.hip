@@ -209,47 +209,48 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
 }
 
 // out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s over the active
-// splits s of head h (grid Hq, HD threads).
+// splits s of head h (grid Hq, HD threads).  The position, the first 64 splits'
+// statistics and the first kMergePf partials of the thread's column are all
+// requested at once (clamped into the split range), so a context of up to
+// kMergePf splits costs one memory round trip; each wavefront reduces the
+// statistics itself (no barrier before the weights exist).
+constexpr int kMergePf = 32;
 template <int HD>
 __global__ __launch_bounds__(HD) void k_attn_merge(const float* __restrict__ part_o,
                                                    const float* __restrict__ part_ml,
                                                    int nsplit, const DecodeState* __restrict__ st,
                                                    float* __restrict__ out) {
   __shared__ float w[kMaxSplits];
-  __shared__ float red[HD / 64];
   const int h = blockIdx.x, d = threadIdx.x, lane = d & 63, wv = d >> 6;
-  const int active = (st->pos + kChunk) / kChunk;  // ceil((pos + 1) / chunk)
   const float* ml = part_ml + (size_t)h * nsplit * 2;
-  float mloc = -INFINITY;
-  for (int s = d; s < active; s += HD) mloc = fmaxf(mloc, ml[2 * s]);
-  mloc = wave_max(mloc);
-  if (lane == 0) red[wv] = mloc;
-  __syncthreads();
-  float M = red[0];
-#pragma unroll
-  for (int i = 1; i < HD / 64; ++i) M = fmaxf(M, red[i]);
-  float lsum = 0.f;
-  for (int s = d; s < active; s += HD) {
-    const float e = __expf(ml[2 * s] - M);
-    w[s] = e;
-    lsum += e * ml[2 * s + 1];
-  }
-  lsum = wave_sum(lsum);
-  __syncthreads();
-  if (lane == 0) red[wv] = lsum;
-  __syncthreads();
-  float L = 0.f;
-#pragma unroll
-  for (int i = 0; i < HD / 64; ++i) L += red[i];
   const float* po = part_o + (size_t)h * nsplit * HD + d;
-  float o = 0.f;
-  int s = 0;
-  for (; s + 4 <= active; s += 4) {
-    const float a0 = po[(size_t)(s + 0) * HD], a1 = po[(size_t)(s + 1) * HD];
-    const float a2 = po[(size_t)(s + 2) * HD], a3 = po[(size_t)(s + 3) * HD];
-    o += w[s] * a0 + w[s + 1] * a1 + w[s + 2] * a2 + w[s + 3] * a3;
+  const int pos = st->pos;
+  const float2 s0 = reinterpret_cast<const float2*>(ml)[min(lane, nsplit - 1)];
+  float pv[kMergePf];
+#pragma unroll
+  for (int k = 0; k < kMergePf; ++k) pv[k] = po[(size_t)min(k, nsplit - 1) * HD];
+  const int active = min((pos + kChunk) / kChunk, nsplit);  // ceil((pos + 1) / chunk)
+  float mloc = lane < active ? s0.x : -INFINITY;
+  for (int s = lane + 64; s < active; s += 64) mloc = fmaxf(mloc, ml[2 * s]);
+  const float M = wave_max(mloc);
+  float lsum = 0.f;
+  if (lane < active) {
+    const float e = __expf(s0.x - M);
+    lsum = e * s0.y;
+    if (wv == 0) w[lane] = e;
   }
-  for (; s < active; ++s) o += w[s] * po[(size_t)s * HD];
+  for (int s = lane + 64; s < active; s += 64) {
+    const float e = __expf(ml[2 * s] - M);
+    lsum += e * ml[2 * s + 1];
+    if (wv == 0) w[s] = e;
+  }
+  const float L = wave_sum(lsum);
+  __syncthreads();
+  float o = 0.f;
+#pragma unroll
+  for (int k = 0; k < kMergePf; ++k)
+    if (k < active) o += w[k] * pv[k];
+  for (int s = kMergePf; s < active; ++s) o += w[s] * po[(size_t)s * HD];
   out[(size_t)h * HD + d] = o / L;
 }
 

@@ -60,14 +60,15 @@ struct QkvRope {
 
 // y = W x for W [N, K] row-major (bf16 bits or fp32), x fp32 [K].
 // norm_gain != nullptr: x is first RMS-normalised (eps) and scaled by the gain.
-// STORE: y[n] = acc.  RESID: y[n] += acc.  SWIGLU: rows (2i, 2i+1) hold
-// (gate_i, up_i) and y[i] = silu(gate_i) * up_i.  ARGMAX: y[n] = acc and one
-// ArgmaxPart per block into `part` (grid size returned through *nblocks).
-// QKV: as described for QkvRope (`rope` required, N = (n_q + 2 n_kv) * hd).
+// RESID: y[n] += acc (norm_gain must be nullptr).  The others take a
+// normalised x (norm_gain required): SWIGLU: rows (2i, 2i+1) hold (gate_i,
+// up_i) and y[i] = silu(gate_i) * up_i.  ARGMAX: y[n] = acc and one ArgmaxPart
+// per workgroup into `part` (at most 1024; the count is returned through
+// *nblocks).  QKV: as described for QkvRope (`rope` required,
+// N = (n_q + 2 n_kv) * hd).  (STORE is a GEMM epilogue only.)
 hipError_t launch_gemv(int wt, int epi, const void* W, int N, int K, const float* x,
                        const float* norm_gain, float eps, float* y, ArgmaxPart* part,
                        int* nblocks, hipStream_t st, const QkvRope* rope = nullptr);
-int gemv_argmax_blocks(int N);
 
 // Final argmax over `n` partials -> st->token; st->pos += advance (or = set_pos
 // when set_pos >= 0); st->bad set when a partial carries index -1 (a logit was

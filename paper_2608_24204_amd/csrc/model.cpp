@@ -75,6 +75,10 @@ bool config_ok(const wici_config* c, std::string* why) {
     return bad("bad prefill_mode");
   if (c->weight_dtype == WICI_F32 && c->prefill_mode != WICI_PREFILL_F32)
     return bad("fp32 weights need prefill_mode WICI_PREFILL_F32");
+  // the decode GEMV keeps each lane's slices of x in registers
+  if (c->weight_dtype == WICI_F32 &&
+      (c->d_model > 16384 || c->ffn_dim > 16384 || c->n_heads * c->head_dim > 16384))
+    return bad("fp32 weights need d_model, ffn_dim and n_heads*head_dim of at most 16384");
   if (c->flags & ~WICI_FLAG_NO_GRAPH) return bad("unknown flags");
   if (c->tied_embeddings != 0 && c->tied_embeddings != 1) return bad("tied_embeddings must be 0 or 1");
   return true;

@@ -8,7 +8,8 @@ Logits: per step, max_i |g_i - o_i| / max_i |o_i| <= tol.
 Near ties: at a step whose ids differ, the divergence is called a near tie when
 the oracle's own margin between its token and the GPU's token is within twice the
 largest logit error of that step (both tokens are then defensible); it is
-reported, never counted as a pass of the strict criterion.
+reported, never counted as a pass of the strict criterion.  `adjudicated` is the
+weaker verdict: every divergent step is such a near tie.
 """
 
 from __future__ import annotations
@@ -38,10 +39,16 @@ class ParityReport:
     max_rel_err: float = 0.0
     worst_step: int = -1
     min_margin: float = float("inf")
+    divergent: int = 0
+
+    @property
+    def adjudicated(self) -> bool:
+        return len(self.near_ties) == self.divergent
 
     def summary(self) -> dict:
         return {"steps": self.steps, "strict_ids": self.strict_ids,
-                "first_divergence": self.first_divergence, "near_ties": len(self.near_ties),
+                "first_divergence": self.first_divergence, "divergent": self.divergent,
+                "near_ties": len(self.near_ties), "adjudicated": self.adjudicated,
                 "max_rel_err": self.max_rel_err, "min_oracle_margin": self.min_margin}
 
 
@@ -64,6 +71,7 @@ def compare(gpu_ids, gpu_logits, ora_logits) -> ParityReport:
             if rep.first_divergence is None:
                 rep.first_divergence = s
             rep.strict_ids = False
+            rep.divergent += 1
             margin = float(o[otok] - o[gpu_ids[s]])
             if err is not None and margin <= 2 * err:
                 rep.near_ties.append((s, margin, 2 * err))

@@ -7,7 +7,13 @@ each step is teacher-forced on the GPU's own ids).
 The 1B- and 8B-shaped configurations run by default, with bf16 weights and with
 block-scaled 8-bit weights (the oracle then runs on its own quantisation of the
 same bf16 weights); the long-context 8B and the 32B shapes (minutes of float64
-host work each) run when WICI_FULL_PARITY=all."""
+host work each) run when WICI_FULL_PARITY=all.
+
+The five workload configurations of the method must meet the strict criterion
+(every greedy id equal to the oracle's).  The 8-bit variants are held to the
+adjudicated one: any divergent step must be a near tie, the oracle's margin
+between the two tokens within twice that step's largest logit error (both
+verdicts are recorded)."""
 
 from __future__ import annotations
 
@@ -75,5 +81,8 @@ def test_full_size_greedy_run_matches_oracle(cuda_ok, name, mode):
     with open(_report_path(), "a") as f:
         f.write(json.dumps(rec) + "\n")
     assert rep.max_rel_err <= 2e-2, rec
-    assert rep.strict_ids, rec
+    if cfg.weight_dtype == "q8":
+        assert rep.adjudicated, rec
+    else:
+        assert rep.strict_ids, rec
     assert ids_n == [int(i) for i in ids], "wici_decode_n differs from wici_decode_step"
