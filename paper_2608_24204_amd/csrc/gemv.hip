@@ -342,9 +342,10 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
 
 // Launch shape: J = ceil(K / (256 EPL)) units per row, rounded up to an
 // instantiated count (1-8, 10, 12, 14, 16; fp32 and Q8 up to 8); two workgroups
-// per CU; a workgroup with at most 8 groups double-buffers them (its groups'
-// round trips would otherwise follow one another), one with more streams them
-// one at a time (double buffering there puts too many bytes in flight).  (From
+// per CU; a workgroup with at most 8 groups double-buffers them when the two
+// buffers fit the registers (its groups' round trips would otherwise follow one
+// another), one with more groups streams them one at a time (double buffering
+// there puts too many bytes in flight).  (From
 // sweeps of 256..1536 workgroups and single or double buffering over the
 // decode matrices of the 8B shape.)
 struct GemvCfg {
@@ -416,10 +417,14 @@ template <typename WT, int EPI>
 static hipError_t gemv_dispatch(const GemvCfg& cf, const WT* W, int N, int K, const float* x,
                                 const float* gain, float eps, float* y, ArgmaxPart* part,
                                 int* nblocks, hipStream_t st, const QkvRope& rp) {
+  // double buffering for up to 8 units per row (4 for Q8, whose units are twice
+  // as wide in x; beyond that two groups' loads do not fit the registers)
+  constexpr int kDbMaxJ = sizeof(WT) == 1 ? 4 : 8;
 #define WICI_J(JJ)                                                                    \
   case JJ:                                                                            \
-    return cf.db ? gemv_go<WT, EPI, JJ, true>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp) \
-                 : gemv_go<WT, EPI, JJ, false>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp)
+    return cf.db && JJ <= kDbMaxJ                                                     \
+               ? gemv_go<WT, EPI, JJ, (JJ <= kDbMaxJ)>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp) \
+               : gemv_go<WT, EPI, JJ, false>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp)
   switch (cf.J) {
     WICI_J(1); WICI_J(2); WICI_J(3); WICI_J(4); WICI_J(5); WICI_J(6); WICI_J(7); WICI_J(8);
     WICI_J(10); WICI_J(12); WICI_J(14); WICI_J(16);
