@@ -95,10 +95,12 @@ __device__ __forceinline__ float dot16r(const Vec8<uint8_t>& v, const float (&x)
 
 // Rows per group for J units per row: 4-8 loads per lane per group, R even for
 // SwiGLU (gate/up pairs), R = 2 for QKV (RoPE pairs).
-__host__ __device__ constexpr int gemv_rows(int epi, int J) {
+// (Q8 rows of up to 4096 codes are one unit: 8 rows per group, 4 for SwiGLU,
+// which double-buffers instead; measured on the 8B matrices.)
+__host__ __device__ constexpr int gemv_rows(int epi, int J, bool q8 = false) {
   return epi == GEMV_QKV ? 2
          : epi == GEMV_SWIGLU ? (J == 1 ? 4 : 2)
-         : (J == 1 ? 4 : J <= 4 ? 2 : 1);
+         : (J == 1 ? (q8 ? 8 : 4) : J <= 4 ? 2 : 1);
 }
 
 template <typename WT, int EPI, int J, bool DB>
@@ -109,7 +111,7 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
                                               ArgmaxPart* __restrict__ part, int max_rows,
                                               QkvRope rope,
                                               const unsigned short* __restrict__ S) {
-  constexpr int R = gemv_rows(EPI, J);
+  constexpr int R = gemv_rows(EPI, J, sizeof(WT) == 1);
   constexpr bool NORM = EPI != GEMV_RESID;   // the residual GEMVs take x as is
   constexpr bool Q8 = sizeof(WT) == 1;
   constexpr int EPL = LaneElems<WT>::n, SPAN = 256 * EPL, NF4 = EPL / 4;
@@ -342,8 +344,8 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
 
 // Launch shape: J = ceil(K / (256 EPL)) units per row, rounded up to an
 // instantiated count (1-8, 10, 12, 14, 16; fp32 and Q8 up to 8); two workgroups
-// per CU; a workgroup with at most 8 groups double-buffers them when the two
-// buffers fit the registers (its groups' round trips would otherwise follow one
+// per CU; a workgroup with at most 8 groups (16 for Q8) double-buffers them
+// when the two buffers fit the registers (its groups' round trips would otherwise follow one
 // another), one with more groups streams them one at a time (double buffering
 // there puts too many bytes in flight).  (From
 // sweeps of 256..1536 workgroups and single or double buffering over the
@@ -365,11 +367,11 @@ static int gemv_units(int wt, int K) {
 static GemvCfg gemv_cfg(int wt, int epi, int N, int K) {
   GemvCfg c{};
   c.J = gemv_units(wt, K);
-  const int R = gemv_rows(epi, c.J);
+  const int R = gemv_rows(epi, c.J, wt == W_Q8);
   const int ngroups = epi == GEMV_QKV ? N / 2 : (N + R - 1) / R;
   c.grid = std::max(1, std::min(512, ngroups));
   c.max_rows = (ngroups + c.grid - 1) / c.grid * R;
-  c.db = c.max_rows / R <= 8;
+  c.db = c.max_rows / R <= (wt == W_Q8 ? 16 : 8);
   c.lds = (size_t)4 * c.max_rows * sizeof(float);
   return c;
 }
@@ -400,7 +402,7 @@ static hipError_t gemv_go(const GemvCfg& cf, const WT* W, int N, int K, const fl
     (void)hipGetLastError();
     GemvCfg c = cf;
     if (resident > 0 && c.grid > resident) {
-      const int R = gemv_rows(EPI, J);
+      const int R = gemv_rows(EPI, J, sizeof(WT) == 1);
       const int ngroups = EPI == GEMV_QKV ? N / 2 : (N + R - 1) / R;
       c.grid = resident;
       c.max_rows = (ngroups + c.grid - 1) / c.grid * R;
