@@ -36,7 +36,8 @@ __device__ __forceinline__ size_t kv_off(const KvLayout& kv, int pos, int which,
 // splits.  (Merging in the last block of each head would need device-scope
 // fences, whose L2 write-back and invalidate on every block cost more than the
 // extra launch.)
-constexpr int kChunk = 64;       // positions per decode split
+constexpr int kChunk = 64;       // positions per decode split (at most one per lane of a wave:
+                                 // the softmax statistics take one position per lane)
 constexpr int kMaxSplits = 256;  // splits the merge kernel holds in LDS
 
 // With seqs != nullptr the launch is batched: blockIdx.z is the sequence, whose
