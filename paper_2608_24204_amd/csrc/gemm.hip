@@ -24,6 +24,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <algorithm>
+
 namespace wici {
 
 // ------------------------------------------------------------------ epilogue
@@ -59,7 +61,7 @@ __device__ __forceinline__ int lds_chunk(int row, int chunk) {
 template <int NT, int WM, int WN, int EPI, bool Q8>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
     const bf16_t* __restrict__ A, size_t a_plane, int lda, const void* __restrict__ Wv, int M,
-    int N, int K, float* __restrict__ C, int ldc, ActBuf H, int ldh,
+    int N, int K, int ks, float* __restrict__ C, size_t c_split, int ldc, ActBuf H, int ldh,
     const unsigned short* __restrict__ S) {
   constexpr int BM = 64 * WM, BN = 64 * WN, NTH = 64 * WM * WN;
   constexpr int A_CHUNKS = NT * BM * (kBK / 8);  // 16-byte chunks per step
@@ -79,6 +81,10 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
   const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (t >= T) return;
   const int m0 = (t / n_nt) * BM, n0 = (t % n_nt) * BN;
+  // split K: block row y of the grid takes K range [y ks, (y + 1) ks) and writes
+  // its own output (c_split elements further on)
+  const int kbeg = blockIdx.y * ks;
+  C += blockIdx.y * c_split;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave / WN, wn = wave % WN;
@@ -91,7 +97,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
       if (c < A_CHUNKS) {
         const int p = c / (BM * 4), row = (c / 4) % BM, part = c % 4;
         const int m = m0 + row;
-        ra[i] = m < M ? *reinterpret_cast<const uint4*>(A + p * a_plane + (size_t)m * lda + k0 + part * 8)
+        ra[i] = m < M ? *reinterpret_cast<const uint4*>(A + p * a_plane + (size_t)m * lda + kbeg + k0 + part * 8)
                       : make_uint4(0, 0, 0, 0);
       }
     }
@@ -101,10 +107,10 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
       if (c < W_CHUNKS) {
         const int row = c / WCPR, part = c % WCPR, n = n0 + row;
         if (Q8)
-          rw[i] = n < N ? *reinterpret_cast<const uint4*>(Wq + (size_t)n * K + k0 + part * 16)
+          rw[i] = n < N ? *reinterpret_cast<const uint4*>(Wq + (size_t)n * K + kbeg + k0 + part * 16)
                         : make_uint4(0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u);
         else
-          rw[i] = n < N ? *reinterpret_cast<const uint4*>(W + (size_t)n * K + k0 + part * 8)
+          rw[i] = n < N ? *reinterpret_cast<const uint4*>(W + (size_t)n * K + kbeg + k0 + part * 8)
                         : make_uint4(0, 0, 0, 0);
       }
     }
@@ -118,7 +124,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = min(n0 + wn * 64 + j * 16 + fr, N - 1);
-      scq[j] = S[(size_t)n * (K / 32) + kt];
+      scq[j] = S[(size_t)n * (K / 32) + kbeg / 32 + kt];
     }
   };
   auto sfix = [&]() {
@@ -166,7 +172,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int KT = K / kBK;
+  const int KT = ks / kBK;
   if (Q8) sload(0);
   gload(0);
   sstore(0);
@@ -412,7 +418,8 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, i
 // ------------------------------------------------------------------- launchers
 template <int NT, int WM, int WN, int EPI, bool Q8>
 static hipError_t gemm_mfma_launch(const ActBuf& A, int lda, const void* W, int M, int N, int K,
-                                   float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
+                                   float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st,
+                                   int nsplit = 1, size_t c_split = 0) {
   constexpr int BM = 64 * WM, BN = 64 * WN;
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   const int grid = (tiles + 7) / 8 * 8;
@@ -425,8 +432,8 @@ static hipError_t gemm_mfma_launch(const ActBuf& A, int lda, const void* W, int 
   if (lds > 65536)
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  hipLaunchKernelGGL(fn, dim3(grid), dim3(64 * WM * WN), lds, st, A.planes, A.plane_stride, lda,
-                     W, M, N, K, C, ldc, H, ldh, S);
+  hipLaunchKernelGGL(fn, dim3(grid, nsplit), dim3(64 * WM * WN), lds, st, A.planes,
+                     A.plane_stride, lda, W, M, N, K, K / nsplit, C, c_split, ldc, H, ldh, S);
   return hipGetLastError();
 }
 
@@ -491,6 +498,32 @@ static hipError_t gemm_f32(const ActBuf& A, int lda, const WT* W, int M, int N, 
   hipLaunchKernelGGL((k_gemm_f32<WT, EPI>), grid, dim3(256), 0, st, A.f32, lda, W, M, N, K, C,
                      ldc, H, ldh, S);
   return hipGetLastError();
+}
+
+// Split K for products with too few output tiles to fill the chip: as many
+// splits as still leave at most two blocks per CU (512), each at least 256 deep.
+int gemm_split_count(int wt, int nt, int M, int N, int K, int max_split) {
+  if (nt < 1 || M <= 32 || (wt != W_BF16 && wt != W_Q8)) return 1;
+  const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  int n = std::max(1, std::min(max_split, 512 / std::max(tiles, 1)));
+  while (n > 1 && (K % (kBK * n) || K / n < 256)) --n;
+  return n;
+}
+
+hipError_t launch_gemm_split(int wt, const ActBuf& A, int lda, const void* W, int M, int N, int K,
+                             int nsplit, float* P, size_t p_split, hipStream_t st) {
+  if (nsplit < 1 || K % (kBK * nsplit) || A.nt < 1 || A.nt > 3 || M <= 32 ||
+      (wt != W_BF16 && wt != W_Q8))
+    return hipErrorInvalidValue;
+  const ActBuf none{};
+#define WICI_SP(NT_)                                                                         case NT_:                                                                                    return wt == W_Q8 ? gemm_mfma_launch<NT_, 2, 2, GEMV_STORE, true>(A, lda, W, M, N, K, P,                                                                       N, none, 0, st, nsplit, p_split)                       : gemm_mfma_launch<NT_, 2, 2, GEMV_STORE, false>(A, lda, W, M, N, K, P,                                                                        N, none, 0, st, nsplit, p_split)
+  switch (A.nt) {
+    WICI_SP(1);
+    WICI_SP(2);
+    WICI_SP(3);
+    default: return hipErrorInvalidValue;
+  }
+#undef WICI_SP
 }
 
 hipError_t launch_gemm(int wt, int epi, const ActBuf& A, int lda, const void* W, int M, int N,

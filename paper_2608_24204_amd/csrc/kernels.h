@@ -151,5 +151,17 @@ bool attn_group_supported(int G);
 hipError_t launch_gemm(int wt, int epi, const ActBuf& A, int lda, const void* W, int M,
                        int N, int K, float* C, int ldc, const ActBuf& H, int ldh,
                        hipStream_t st);
+// The same product (matrix cores, nt >= 1, M > 32) over nsplit K ranges of equal
+// depth (K a multiple of 32 nsplit): range s writes P + s * p_split ([M, N], row
+// stride N, fp32).  gemm_split_count picks nsplit (1: do not split).
+hipError_t launch_gemm_split(int wt, const ActBuf& A, int lda, const void* W, int M, int N, int K,
+                             int nsplit, float* P, size_t p_split, hipStream_t st);
+int gemm_split_count(int wt, int nt, int M, int N, int K, int max_split);
+// x[t] += sum over s < nsplit of P[s * p_split + t * d] (in that order) for T rows
+// of width d; then, with gain != nullptr, y[t] = RMSNorm(x[t]) * gain (as
+// launch_rmsnorm_rows).
+hipError_t launch_resid_sum_rmsnorm(float* x, const float* P, int nsplit, size_t p_split,
+                                    const float* gain, float eps, int T, int d, const ActBuf& y,
+                                    hipStream_t st);
 
 }  // namespace wici

@@ -138,6 +138,47 @@ hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int
   return hipGetLastError();
 }
 
+// Residual add of split-K partial products, then (optionally) the row RMSNorm.
+__global__ __launch_bounds__(256) void k_resid_sum_rmsnorm(float* __restrict__ x,
+                                                           const float* __restrict__ P,
+                                                           int nsplit, size_t p_split,
+                                                           const float* __restrict__ g,
+                                                           float eps, int d, ActBuf y) {
+  __shared__ float red[4];
+  float* xr = x + (size_t)blockIdx.x * d;
+  const float* pr = P + (size_t)blockIdx.x * d;
+  const size_t yr = (size_t)blockIdx.x * d;
+  float ss = 0.f;
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    float4 v = *reinterpret_cast<const float4*>(xr + k);
+    for (int s = 0; s < nsplit; ++s) {
+      const float4 p = *reinterpret_cast<const float4*>(pr + s * p_split + k);
+      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+    }
+    *reinterpret_cast<float4*>(xr + k) = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  if (!g) return;
+  const float r = 1.0f / sqrtf(block256_sum(ss, red) / (float)d + eps);
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {  // this thread's own values
+    const float4 v = *reinterpret_cast<const float4*>(xr + k);
+    const float4 w = *reinterpret_cast<const float4*>(g + k);
+    store_act(y, yr + k + 0, v.x * r * w.x);
+    store_act(y, yr + k + 1, v.y * r * w.y);
+    store_act(y, yr + k + 2, v.z * r * w.z);
+    store_act(y, yr + k + 3, v.w * r * w.w);
+  }
+}
+
+hipError_t launch_resid_sum_rmsnorm(float* x, const float* P, int nsplit, size_t p_split,
+                                    const float* gain, float eps, int T, int d, const ActBuf& y,
+                                    hipStream_t st) {
+  if (nsplit < 1 || d % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_resid_sum_rmsnorm, dim3(T), dim3(256), 0, st, x, P, nsplit, p_split, gain,
+                     eps, d, y);
+  return hipGetLastError();
+}
+
 // ---- RoPE + KV append for prefill rows --------------------------------------------
 // One block per row; thread j < hd/2 of a head rotates the pair (j, j + hd/2).
 template <typename KT>

@@ -28,6 +28,7 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kMaxGemvBlocks = 1024;
 constexpr int kMaxBatch = 256;  // sequences per batched decode step
+constexpr int kMaxKSplit = 4;   // K ranges of a prefill residual product (partials kept)
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 size_t dsize(int32_t dt) { return dt == WICI_BF16 ? 2 : 4; }
@@ -40,7 +41,8 @@ struct Layout {
   int n_pages;
   size_t kv_layer_stride, kv_bytes;
   // scratch
-  size_t x, a, qkv, att, h, logits, parts, part_o, part_ml, tokens, table, state, hist, seqs;
+  size_t x, a, qkv, att, h, kpart, logits, parts, part_o, part_ml, tokens, table, state, hist,
+      seqs;
   size_t scratch_bytes;
   int nsplit;
 };
@@ -126,6 +128,7 @@ Layout make_layout(const wici_config& c) {
   L.qkv = o; o = align_up(o + C * nqkv * 4);
   L.att = o; o = align_up(o + C * qd * 6);
   L.h = o; o = align_up(o + C * F * 6);
+  L.kpart = o; o = align_up(o + (size_t)kMaxKSplit * C * d * 4);  // split-K partials
   L.logits = o; o = align_up(o + V * 4);
   L.parts = o; o = align_up(o + kMaxGemvBlocks * sizeof(ArgmaxPart));
   L.part_o = o; o = align_up(o + (size_t)c.n_heads * L.nsplit * c.head_dim * 4);
@@ -345,10 +348,27 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   if ((e = wici::launch_embed(wb, m->dw + L.embed, c.vocab, d, m->S<int32_t>(L.tokens), T, nullptr,
                               x, s)))
     return e;
+  // The residual products (O, down) have only d output columns: with few rows
+  // they are split along K into partials that the next row RMSNorm adds to x
+  // (in split order, so the result does not depend on scheduling).
+  float* P = m->S<float>(L.kpart);
+  const size_t p_split = C * d;
+  const int s_o = wici::gemm_split_count(wb, nt, T, d, qd, kMaxKSplit);
+  const int s_d = wici::gemm_split_count(wb, nt, T, d, F, kMaxKSplit);
+  int pending = 0;  // splits of the previous down product not yet added to x
+  auto norm = [&](const float* gain, int nsplit) {
+    return nsplit > 1 ? wici::launch_resid_sum_rmsnorm(x, P, nsplit, p_split, gain, c.rms_eps, T,
+                                                       d, a, s)
+                      : wici::launch_rmsnorm_rows(x, gain, c.rms_eps, T, d, a, s);
+  };
+  auto resid = [&](const wici::ActBuf& in, int K, size_t w, int nsplit) {
+    return nsplit > 1 ? wici::launch_gemm_split(wb, in, K, m->dw + w, T, d, K, nsplit, P, p_split,
+                                                s)
+                      : wici::launch_gemm(wb, wici::GEMV_RESID, in, K, m->dw + w, T, d, K, x, d,
+                                          none, 0, s);
+  };
   for (int l = 0; l < c.n_layers; ++l) {
-    if ((e = wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, T, d,
-                                       a, s)))
-      return e;
+    if ((e = norm(m->W<float>(m->layer(l, L.l_anorm)), pending))) return e;
     if ((e = wici::launch_gemm(wb, wici::GEMV_STORE, a, d, m->dw + m->layer(l, L.l_wqkv), T,
                                nqkv, d, qkv, nqkv, none, 0, s)))
       return e;
@@ -356,19 +376,16 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
                                       m->W<float>(L.rope_sin), m->kv(l), s)))
       return e;
     if ((e = wici::launch_attn_prefill(kb, qkv, T, p0, c.n_heads, m->kv(l), att, s))) return e;
-    if ((e = wici::launch_gemm(wb, wici::GEMV_RESID, att, qd, m->dw + m->layer(l, L.l_wo), T, d,
-                               qd, x, d, none, 0, s)))
-      return e;
-    if ((e = wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_fnorm)), c.rms_eps, T, d,
-                                       a, s)))
-      return e;
+    if ((e = resid(att, qd, m->layer(l, L.l_wo), s_o))) return e;
+    if ((e = norm(m->W<float>(m->layer(l, L.l_fnorm)), s_o))) return e;
     if ((e = wici::launch_gemm(wb, wici::GEMV_SWIGLU, a, d, m->dw + m->layer(l, L.l_wgu), T,
                                2 * F, d, nullptr, 0, h, F, s)))
       return e;
-    if ((e = wici::launch_gemm(wb, wici::GEMV_RESID, h, F, m->dw + m->layer(l, L.l_wdown), T, d, F,
-                               x, d, none, 0, s)))
-      return e;
+    if ((e = resid(h, F, m->layer(l, L.l_wdown), s_d))) return e;
+    pending = s_d;
   }
+  if (pending > 1)
+    return wici::launch_resid_sum_rmsnorm(x, P, pending, p_split, nullptr, 0.f, T, d, a, s);
   return hipSuccess;
 }
 
