@@ -37,15 +37,18 @@ def prompts(cfg, n):
     return [rng.integers(0, cfg.vocab, cfg.prompt_len - 9 * b).astype(np.int32) for b in range(n)]
 
 
+@pytest.mark.parametrize("cap", [None, 5000], ids=["cap_default", "cap5000"])
 @pytest.mark.parametrize("kind", list(CFGS))
-def test_batched_decode_matches_oracle_per_sequence(cuda_ok, kind):
+def test_batched_decode_matches_oracle_per_sequence(cuda_ok, kind, cap):
+    """cap5000: a capacity above 2048 positions, where each decode-attention
+    block walks several 64-position sub-chunks."""
     cfg = CFGS[kind]
     w = inputs.make_weights(cfg, gain_std=0.1)
     w64 = inputs.weights_f64(cfg, w)
     tol = 1e-4 if cfg.weight_dtype == "f32" else 2e-2
     n = 4
     ps = prompts(cfg, n)
-    ms = clients(cfg, w, n, kv_page=16)
+    ms = clients(cfg, w, n, kv_page=16, **({"max_seq": cap} if cap else {}))
     try:
         ids = [[] for _ in range(n)]
         logs = [[] for _ in range(n)]

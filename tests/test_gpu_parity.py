@@ -96,6 +96,19 @@ def test_ragged_prompts_chunks_and_pages(cuda_ok, P, chunk, page):
     assert rep.strict_ids, rep.summary()
 
 
+@pytest.mark.parametrize("P,max_seq,page", [(2100, 2200, 16), (2600, 4096, 64),
+                                              (3000, 9000, 16), (5000, 16384, 128)])
+def test_long_capacity_decode_attention(cuda_ok, P, max_seq, page):
+    """Capacities above 2048 positions give each decode-attention block several
+    64-position sub-chunks (2, 2, 5 and 8 here) under one online softmax, and the
+    merge fewer, longer splits."""
+    cfg = SMALL["gqa128_bf16"]
+    prompt = inputs.make_prompt(cfg, P)
+    rep, _, _ = run_parity(cfg, prompt, 12, gain_std=0.1, kv_page=page, max_seq=max_seq)
+    assert rep.max_rel_err <= 2e-2
+    assert rep.strict_ids, rep.summary()
+
+
 @pytest.mark.parametrize("mode", ["bf16x3", "bf16x2", "bf16", "f32"])
 def test_prefill_modes(cuda_ok, mode):
     cfg = SMALL["gqa64_bf16"]
