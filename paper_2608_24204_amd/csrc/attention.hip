@@ -19,7 +19,8 @@ namespace wici {
 constexpr int kMaxGroup = 8;   // query heads per KV head
 
 __device__ __forceinline__ size_t kv_off(const KvLayout& kv, int pos, int which, int h) {
-  const int phys = kv.table[pos / kv.page], slot = pos % kv.page;
+  const int ps = __ffs(kv.page) - 1;  // pages are a power of two
+  const int phys = kv.table[pos >> ps], slot = pos & (kv.page - 1);
   return ((((size_t)phys * 2 + which) * kv.n_kv + h) * kv.page + slot) * (size_t)kv.hd;
 }
 
@@ -79,12 +80,13 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
   const int start = split * kChunk;
   const KT* base = static_cast<const KT*>(kv.base);
   const size_t head_stride = (size_t)kv.page * HD;
+  const int ps = __ffs(kv.page) - 1;  // pages are a power of two
   // page of each of this lane's positions (clamped into the table)
   int phys[NP];
 #pragma unroll
   for (int i = 0; i < NP; ++i) {
     const int j = start + i * PPB + wave * PPW + pg;
-    phys[i] = kv.table[min(j, kv.max_pos - 1) / kv.page];
+    phys[i] = kv.table[min(j, kv.max_pos - 1) >> ps];
   }
   // queries of the group (independent of the position)
   float qv[(G * HD + 255) / 256];
@@ -102,7 +104,7 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
   for (int i = 0; i < NP; ++i) {
     const int j = start + i * PPB + wave * PPW + pg;
     const KT* pk = base + (((size_t)phys[i] * 2 + 0) * Hkv + g) * head_stride +
-                   (size_t)(j % kv.page) * HD + sub * 8;
+                   (size_t)(j & (kv.page - 1)) * HD + sub * 8;
     load8(pk, kr[i]);
     load8(pk + (size_t)Hkv * head_stride, vr[i]);
   }
@@ -352,7 +354,7 @@ hipError_t launch_attn_decode_batch(bool kv_bf16, const float* q, int q_stride, 
                                     float* part_o, float* part_ml, const ActBuf& out,
                                     hipStream_t s) {
   if (B < 1 || nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos || kv.n_kv < 1 ||
-      Hq % kv.n_kv)
+      Hq % kv.n_kv || kv.page < 1 || (kv.page & (kv.page - 1)))
     return hipErrorInvalidValue;
   const int G = Hq / kv.n_kv;
   if (kv.hd == 128) {
@@ -372,7 +374,8 @@ bool attn_group_supported(int G) { return G == 1 || G == 2 || G == 4 || G == 5 |
 hipError_t launch_attn_decode(bool kv_bf16, const float* q, int Hq, KvLayout kv,
                               const void* state, int nsplit, float* part_o, float* part_ml,
                               float* out, hipStream_t s) {
-  if (nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos || kv.n_kv < 1 || Hq % kv.n_kv)
+  if (nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos || kv.n_kv < 1 || Hq % kv.n_kv ||
+      kv.page < 1 || (kv.page & (kv.page - 1)))
     return hipErrorInvalidValue;
   const DecodeState* st = static_cast<const DecodeState*>(state);
   const int G = Hq / kv.n_kv;
@@ -490,6 +493,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   const int width = (Hq + 2 * Hkv) * HD;
   const bf16_t* base = static_cast<const bf16_t*>(kv.base);
   const size_t head_stride = (size_t)kv.page * HD;
+  const int ps = __ffs(kv.page) - 1;  // pages are a power of two
 
   // ---- this lane's query (B operand of S^T = K Q^T): row l16 of the wavefront ----
   const int tq = qb + wave * 16 + l16;        // query row in the chunk
@@ -533,9 +537,9 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
         for (int u = 0; u < 2; ++u) {
           const int j = kb + 2 * pr + u;
           if (j < kend) {
-            const int pp = kv.table[j / kv.page];
+            const int pp = kv.table[j >> ps];
             const bf16_t* kp = base + (((size_t)pp * 2 + 0) * Hkv + g) * head_stride +
-                               (size_t)(j % kv.page) * HD + ch * 16;
+                               (size_t)(j & (kv.page - 1)) * HD + ch * 16;
             const bf16_t* vp = kp + (size_t)Hkv * head_stride;
             rk[it][u][0] = *reinterpret_cast<const uint4*>(kp);
             rk[it][u][1] = *reinterpret_cast<const uint4*>(kp + 8);
@@ -696,6 +700,7 @@ static hipError_t attn_prefill_mfma(const float* qkv, int T, int p0, int Hq, KvL
 // vector kernel.
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
                                KvLayout kv, const ActBuf& out, hipStream_t s) {
+  if (kv.page < 1 || (kv.page & (kv.page - 1))) return hipErrorInvalidValue;
   if (kv_bf16 && out.nt >= 1) {
     if (kv.hd == 128) return attn_prefill_mfma<128>(qkv, T, p0, Hq, kv, out, s);
     if (kv.hd == 64) return attn_prefill_mfma<64>(qkv, T, p0, Hq, kv, out, s);
