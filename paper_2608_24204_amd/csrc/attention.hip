@@ -211,6 +211,192 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
   }
 }
 
+// The same split (64 positions of one KV head, all G query heads) on the matrix
+// cores, for a bf16 cache.  Wavefront w takes positions 16 w .. 16 w + 15 of the
+// split.  S^T = K Q^T on v_mfma_f32_16x16x32_bf16: lane l's 16 bytes of keys
+// (position l % 16, dimensions 8 (l / 16) + 32 s) are exactly its A operand, the
+// query heads are the 16 columns (zero past G) and the fp32 query enters as
+// three bf16 terms accumulated into the same tile, so the scores keep fp32
+// precision.  The result leaves lane l with 4 positions of head l % 16, which is
+// the A-operand order of P V on v_mfma_f32_16x16x16_bf16 (the probabilities
+// again as three bf16 terms); the values go through LDS transposed to
+// [dimension][position] for the B operand.  Each wavefront keeps its own
+// (max, sum) per head; one barrier, then the four are combined and the split's
+// unnormalised output and statistics written as by k_attn_decode.
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+
+template <int HD, int G>
+__global__ __launch_bounds__(256) void k_attn_decode_mfma(const float* __restrict__ q_in,
+                                                          KvLayout kv,
+                                                          const DecodeState* __restrict__ st,
+                                                          float* __restrict__ part_o,
+                                                          float* __restrict__ part_ml,
+                                                          const SeqDesc* __restrict__ seqs,
+                                                          int layer, int q_stride) {
+  static_assert(G <= 16, "query heads are the 16 columns of a tile");
+  if (seqs) {
+    const SeqDesc sd = seqs[blockIdx.z];
+    kv.base = static_cast<char*>(sd.kv) + (size_t)layer * sd.kv_layer_stride;
+    kv.table = sd.table;
+    st = static_cast<const DecodeState*>(sd.state);
+    q_in += (size_t)blockIdx.z * q_stride;
+    const size_t heads = (size_t)kv.n_kv * G * gridDim.x;
+    part_o += (size_t)blockIdx.z * heads * HD;
+    part_ml += (size_t)blockIdx.z * heads * 2;
+  }
+  constexpr int DS = HD / 32;  // 32-deep steps of S^T
+  constexpr int DT = HD / 16;  // 16-wide output tiles of P V
+  constexpr int VP = 16 + 4;   // LDS row of one dimension's 16 positions (8-byte aligned reads)
+  __shared__ bf16_t vt[4][HD][VP];
+  __shared__ float wm[4][G], wl[4][G];
+  __shared__ float wo[4][G][HD];
+
+  const int nsplit = gridDim.x, split = blockIdx.x, g = blockIdx.y;
+  const int Hkv = kv.n_kv;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int start = split * kChunk;
+  const int ps = __ffs(kv.page) - 1;
+  const bf16_t* base = static_cast<const bf16_t*>(kv.base);
+  const size_t head_stride = (size_t)kv.page * HD;
+
+  // round trip 1: this lane's page, its query slice (head r16), the position
+  const int jl = start + 16 * wave + r16;  // this lane's key/value position
+  const int jc = min(jl, kv.max_pos - 1);
+  const int phys = kv.table[jc >> ps];
+  float qv[DS][8];
+  {
+    const float* qr = q_in + ((size_t)g * G + min(r16, G - 1)) * HD + 8 * g4;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      const float4 a = *reinterpret_cast<const float4*>(qr + 32 * s);
+      const float4 b = *reinterpret_cast<const float4*>(qr + 32 * s + 4);
+      qv[s][0] = a.x; qv[s][1] = a.y; qv[s][2] = a.z; qv[s][3] = a.w;
+      qv[s][4] = b.x; qv[s][5] = b.y; qv[s][6] = b.z; qv[s][7] = b.w;
+    }
+  }
+  const int n = st->pos + 1;
+  if (start >= n) return;
+
+  // round trip 2: the keys and values of this lane's position
+  const bf16_t* pk = base + (((size_t)phys * 2 + 0) * Hkv + g) * head_stride +
+                     (size_t)(jc & (kv.page - 1)) * HD + 8 * g4;
+  const bf16_t* pv = pk + (size_t)Hkv * head_stride;
+  bf16x8_t kf[DS];
+  uint4 vr[DS];
+#pragma unroll
+  for (int s = 0; s < DS; ++s) {
+    kf[s] = *reinterpret_cast<const bf16x8_t*>(pk + 32 * s);
+    vr[s] = *reinterpret_cast<const uint4*>(pv + 32 * s);
+  }
+  // the query as three bf16 terms (columns past G are zero)
+  bf16x8_t qb[3][DS];
+#pragma unroll
+  for (int s = 0; s < DS; ++s)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float v = r16 < G ? qv[s][e] : 0.f;
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+        const __bf16 b = static_cast<__bf16>(v);
+        qb[t][s][e] = b;
+        v -= static_cast<float>(b);
+      }
+    }
+  // values transposed into this wavefront's LDS tile (zero past the context:
+  // a stale slot may hold anything, and 0 x NaN is NaN)
+  const bool valid = jl < n;
+#pragma unroll
+  for (int s = 0; s < DS; ++s) {
+    const unsigned w4[4] = {vr[s].x, vr[s].y, vr[s].z, vr[s].w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const unsigned w = valid ? w4[e] : 0u;
+      vt[wave][32 * s + 8 * g4 + 2 * e][r16] = (bf16_t)(w & 0xffffu);
+      vt[wave][32 * s + 8 * g4 + 2 * e + 1][r16] = (bf16_t)(w >> 16);
+    }
+  }
+
+  // S^T: lane holds S[position 4 g4 + i][head r16]
+  floatx4_t sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < DS; ++s)
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qb[t][s], sc, 0, 0, 0);
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (start + 16 * wave + 4 * g4 + i >= n) sc[i] = -INFINITY;
+    m = fmaxf(m, sc[i]);
+  }
+  m = fmaxf(m, __shfl_xor(m, 16));
+  m = fmaxf(m, __shfl_xor(m, 32));
+  float p[4], l = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    p[i] = sc[i] == -INFINITY ? 0.f : __expf(sc[i] - m);
+    l += p[i];
+  }
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  // P as three bf16 terms in the A-operand order (head r16, positions 4 g4 + i)
+  short4_t pa[3];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float v = p[i];
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+      const __bf16 b = static_cast<__bf16>(v);
+      pa[t][i] = __builtin_bit_cast(short, b);
+      v -= static_cast<float>(b);
+    }
+  }
+  __syncthreads();  // the value tiles are in LDS
+
+  // O = P V: lane holds O[head 4 g4 + i][dimension 16 u + r16]
+  floatx4_t o[DT];
+#pragma unroll
+  for (int u = 0; u < DT; ++u) {
+    o[u] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    const short4_t vb = *reinterpret_cast<const short4_t*>(&vt[wave][16 * u + r16][4 * g4]);
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+      o[u] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vb, o[u], 0, 0, 0);
+  }
+  // combine the four wavefronts
+  if (g4 == 0 && r16 < G) { wm[wave][r16] = m; wl[wave][r16] = l; }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int h = 4 * g4 + i;
+    if (h < G) {
+#pragma unroll
+      for (int u = 0; u < DT; ++u) wo[wave][h][16 * u + r16] = o[u][i];
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < G * HD; idx += 256) {
+    const int h = idx / HD, d = idx % HD;
+    float M = wm[0][h];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) M = fmaxf(M, wm[w][h]);
+    float acc = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float e = wm[w][h] == -INFINITY ? 0.f : __expf(wm[w][h] - M);
+      acc += e * wo[w][h][d];
+      L += e * wl[w][h];
+    }
+    const int hh = g * G + h;
+    part_o[((size_t)hh * nsplit + split) * HD + d] = acc;
+    if (d == 0) {
+      part_ml[((size_t)hh * nsplit + split) * 2 + 0] = M;
+      part_ml[((size_t)hh * nsplit + split) * 2 + 1] = L;
+    }
+  }
+}
+
 // out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s over the active
 // splits s of head h (grid Hq, HD threads).  The position, the first 64 splits'
 // statistics and the first kMergePf partials of the thread's column are all
@@ -304,8 +490,12 @@ template <int HD, typename KT, int G>
 static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const DecodeState* st,
                                 int nsplit, float* part_o, float* part_ml, float* out,
                                 hipStream_t s) {
-  launch_k(k_attn_decode<HD, KT, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv, st,
-           part_o, part_ml, (const SeqDesc*)nullptr, 0, 0);
+  if constexpr (sizeof(KT) == 2)
+    launch_k(k_attn_decode_mfma<HD, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv,
+             st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0);
+  else
+    launch_k(k_attn_decode<HD, KT, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv,
+             st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0);
   launch_k(k_attn_merge<HD>, dim3(Hq), dim3(HD), 0, s, kLast, part_o, part_ml, nsplit, st, out);
   return hipGetLastError();
 }
@@ -314,8 +504,12 @@ template <int HD, typename KT, int G>
 static hipError_t attn_decode_batch_t(const float* q, int q_stride, int B, int Hq, KvLayout kv,
                                       const SeqDesc* seqs, int layer, int nsplit, float* part_o,
                                       float* part_ml, const ActBuf& out, hipStream_t s) {
-  hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv, B), dim3(256), 0, s, q,
-                     kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer, q_stride);
+  if constexpr (sizeof(KT) == 2)
+    hipLaunchKernelGGL((k_attn_decode_mfma<HD, G>), dim3(nsplit, kv.n_kv, B), dim3(256), 0, s, q,
+                       kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer, q_stride);
+  else
+    hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv, B), dim3(256), 0, s, q,
+                       kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer, q_stride);
   hipLaunchKernelGGL((k_attn_merge_batch<HD>), dim3(Hq, B), dim3(HD), 0, s, part_o, part_ml,
                      nsplit, seqs, out);
   return hipGetLastError();
