@@ -75,9 +75,11 @@ hipError_t launch_gemv(int wt, int epi, const void* W, int N, int K, const float
 // not finite), in which case st->token = -1.  The chosen token is also stored
 // at hist[new pos - 1] (the token that follows that position).  A decode step
 // (advance > 0) that finds st->bad already set changes nothing: once a step of
-// a device-resident run has failed, the steps queued after it are no-ops.
+// a device-resident run has failed, the steps queued after it are no-ops.  With
+// host_mirror != nullptr (pinned host memory holding a DecodeState) the new
+// state is also written there, for the host to read after synchronising.
 hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int32_t* hist,
-                               int advance, int set_pos, hipStream_t st);
+                               int advance, int set_pos, void* host_mirror, hipStream_t st);
 
 // x[t, :] = E[tokens[t], :] for t < T (tokens == nullptr: the state's token, T = 1;
 // a negative state token, left by a failed step, gives a zero row).

@@ -233,7 +233,7 @@ hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
 __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restrict__ part,
                                                         int n, DecodeState* st,
                                                         int32_t* __restrict__ hist, int advance,
-                                                        int set_pos) {
+                                                        int set_pos, DecodeState* mirror) {
   __shared__ float sv[16];
   __shared__ int si[16];
   __shared__ int sbad[16];
@@ -267,13 +267,19 @@ __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restr
     st->token = tok;
     st->pos = pos;
     if (pos >= 1) hist[pos - 1] = tok;
+    if (mirror) {  // pinned host copy, read after the stream's synchronisation
+      mirror->bad = bad;
+      mirror->token = tok;
+      mirror->pos = pos;
+    }
   }
 }
 
 hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int32_t* hist,
-                               int advance, int set_pos, hipStream_t st) {
+                               int advance, int set_pos, void* host_mirror, hipStream_t st) {
   launch_k(k_argmax_final, dim3(1), dim3(1024), 0, st, kOnly, part, n,
-                     static_cast<DecodeState*>(state), hist, advance, set_pos);
+           static_cast<DecodeState*>(state), hist, advance, set_pos,
+           static_cast<DecodeState*>(host_mirror));
   return hipGetLastError();
 }
 

@@ -171,7 +171,8 @@ struct wici_model {
   int32_t pos = 0;
   bool have_token = false;
   bool shared_weights = false;  // weights bound from another model (read-only here)
-  DecodeState* h_state = nullptr;  // pinned staging
+  DecodeState* h_state = nullptr;         // pinned, device-mapped state mirror (host view)
+  DecodeState* d_state_mirror = nullptr;  // the same memory as the kernels address it
   hipGraph_t graph = nullptr;
   hipGraphExec_t gexec = nullptr;
   // batched decode steps led by this model, captured per batch size (the
@@ -313,7 +314,7 @@ hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers 
                               m->W<float>(L.final_norm), c.rms_eps, m->S<float>(L.logits),
                               m->S<ArgmaxPart>(L.parts), &nb, s));
   WICI_STEP(wici::launch_argmax_final(m->S<ArgmaxPart>(L.parts), nb, st, m->S<int32_t>(L.hist), 1,
-                                      -1, s));
+                                      -1, m->d_state_mirror, s));
 #undef WICI_STEP
   return hipSuccess;
 }
@@ -469,9 +470,21 @@ bool same_weights_geometry(const wici_config& a, const wici_config& b) {
          a.max_seq == b.max_seq;
 }
 
+// Pinned host memory that the final argmax kernel writes the step state into
+// (coherent, so the kernel's stores reach it directly), replacing a
+// device-to-host copy per step.
+hipError_t alloc_state_mirror(wici_model* m) {
+  if (m->h_state) return hipSuccess;
+  if (hipError_t e = hipHostMalloc((void**)&m->h_state, sizeof(DecodeState),
+                                   hipHostMallocMapped | hipHostMallocCoherent))
+    return e;
+  *m->h_state = DecodeState{};
+  return hipHostGetDevicePointer((void**)&m->d_state_mirror, m->h_state, 0);
+}
+
+// The step's final argmax kernel has written the new state into the pinned
+// mirror m->h_state as well; it is read once the stream has drained.
 wici_status finish_step(wici_model* m, int32_t* tok, float* logits) {
-  HIP_TRY(m, hipMemcpyAsync(m->h_state, m->ds + m->L.state, sizeof(DecodeState),
-                            hipMemcpyDeviceToHost, m->stream));
   if (logits)
     HIP_TRY(m, hipMemcpyAsync(logits, m->ds + m->L.logits, (size_t)m->cfg.vocab * 4,
                               hipMemcpyDeviceToHost, m->stream));
@@ -557,7 +570,7 @@ wici_status wici_bind_memory(wici_model* m, void* d_weights, size_t weight_bytes
   m->dw = static_cast<char*>(d_weights);
   m->dkv = static_cast<char*>(d_kv);
   m->ds = static_cast<char*>(d_scratch);
-  HIP_TRY(m, hipHostMalloc((void**)&m->h_state, sizeof(DecodeState), hipHostMallocDefault));
+  HIP_TRY(m, alloc_state_mirror(m));
   // RoPE angle table: pos * base^(-2j/hd), evaluated in double, stored as fp32.
   const wici_config& c = m->cfg;
   const int half = c.head_dim / 2;
@@ -734,7 +747,8 @@ wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
                                m->W<float>(L.final_norm), c.rms_eps, m->S<float>(L.logits),
                                m->S<ArgmaxPart>(L.parts), &nb, m->stream));
   HIP_TRY(m, wici::launch_argmax_final(m->S<ArgmaxPart>(L.parts), nb, m->ds + L.state,
-                                       m->S<int32_t>(L.hist), 0, m->pos + n_tokens, m->stream));
+                                       m->S<int32_t>(L.hist), 0, m->pos + n_tokens,
+                                       m->d_state_mirror, m->stream));
   return finish_step(m, first_token, logits);
 }
 
@@ -773,8 +787,6 @@ wici_status wici_decode_n(wici_model* m, int32_t token_in, int32_t n, int32_t* t
   // hist[pos0 .. pos0+n) holds the token emitted after each processed position
   // (-1 from a failed step on); the state says how far the run got.
   HIP_TRY(m, hipMemcpyAsync(tokens_out, m->ds + m->L.hist + (size_t)pos0 * 4, (size_t)n * 4,
-                            hipMemcpyDeviceToHost, m->stream));
-  HIP_TRY(m, hipMemcpyAsync(m->h_state, m->ds + m->L.state, sizeof(DecodeState),
                             hipMemcpyDeviceToHost, m->stream));
   if (logits)
     HIP_TRY(m, hipMemcpyAsync(logits, m->ds + m->L.logits, (size_t)m->cfg.vocab * 4,
@@ -851,7 +863,7 @@ wici_status wici_bind_memory_shared(wici_model* m, const wici_model* src, void* 
   m->dw = src->dw;
   m->dkv = static_cast<char*>(d_kv);
   m->ds = static_cast<char*>(d_scratch);
-  HIP_TRY(m, hipHostMalloc((void**)&m->h_state, sizeof(DecodeState), hipHostMallocDefault));
+  HIP_TRY(m, alloc_state_mirror(m));
   HIP_TRY(m, wici::launch_init_block_table(m->S<int32_t>(m->L.table), m->L.n_pages, m->stream));
   HIP_TRY(m, wici::launch_reset_state(m->ds + m->L.state, m->stream));
   HIP_TRY(m, hipStreamSynchronize(m->stream));
