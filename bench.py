@@ -255,7 +255,7 @@ def main(argv=None):
                                  [0, 0.0625, 1, 16, 64, 256, 4096])
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              f"(this build has no multi-GPU path)", file=sys.stderr)
+              f"(the decode path runs on a single GPU; it has no multi-GPU sharding)", file=sys.stderr)
         return 2
 
     import torch
