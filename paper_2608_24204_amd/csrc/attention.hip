@@ -398,17 +398,18 @@ __global__ __launch_bounds__(256) void k_attn_decode_mfma(const float* __restric
 }
 
 // out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s over the active
-// splits s of head h (grid Hq, HD threads).  The position, the first 64 splits'
-// statistics and the first kMergePf partials of the thread's column are all
-// requested at once (clamped into the split range), so a context of up to
-// kMergePf splits costs one memory round trip; each wavefront reduces the
-// statistics itself (no barrier before the weights exist).
+// splits s of head h, for launches of at most kMergePf splits (grid Hq, HD
+// threads).  The position, the first 64 splits' statistics and the thread's
+// column of every split are requested at once (clamped into the split range), so
+// the merge costs one memory round trip; each wavefront reduces the statistics
+// itself (no barrier before the weights exist).
 constexpr int kMergePf = 32;
 template <int HD>
-__global__ __launch_bounds__(HD) void k_attn_merge(const float* __restrict__ part_o,
-                                                   const float* __restrict__ part_ml,
-                                                   int nsplit, const DecodeState* __restrict__ st,
-                                                   float* __restrict__ out) {
+__global__ __launch_bounds__(HD) void k_attn_merge_head(const float* __restrict__ part_o,
+                                                        const float* __restrict__ part_ml,
+                                                        int nsplit,
+                                                        const DecodeState* __restrict__ st,
+                                                        float* __restrict__ out) {
   __shared__ float w[kMaxSplits];
   const int h = blockIdx.x, d = threadIdx.x, lane = d & 63, wv = d >> 6;
   const float* ml = part_ml + (size_t)h * nsplit * 2;
@@ -441,6 +442,69 @@ __global__ __launch_bounds__(HD) void k_attn_merge(const float* __restrict__ par
     if (k < active) o += w[k] * pv[k];
   for (int s = kMergePf; s < active; ++s) o += w[s] * po[(size_t)s * HD];
   out[(size_t)h * HD + d] = o / L;
+}
+
+// The same merge for launches of more than kMergePf splits.  Workgroup (h, c)
+// merges columns 32 c .. 32 c + 31 (grid Hq x HD/32, 256 threads): thread t
+// takes column t % 32 of splits t / 32, t / 32 + 8, ...  Every partial below the
+// launch's split count and every split's statistics are requested before the
+// position is known (addresses clamped into the split range), so a context of
+// up to kMaxSplits splits costs one memory round trip and the splits' reads are
+// spread over Hq * HD/32 workgroups.  Each wavefront reduces the statistics itself; slots of inactive
+// splits are skipped, not weighted by zero (they may hold anything).
+constexpr int kMergeRows = 8;                     // split rows of a workgroup
+constexpr int kMergeK = kMaxSplits / kMergeRows;  // partials per thread
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_merge_cols(const float* __restrict__ part_o,
+                                                         const float* __restrict__ part_ml,
+                                                         int nsplit,
+                                                         const DecodeState* __restrict__ st,
+                                                         float* __restrict__ out) {
+  static_assert(HD % 32 == 0, "32-column slices");
+  __shared__ float w[kMaxSplits];
+  __shared__ float red[4][32];
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c = tid & 31, r = tid >> 5;
+  const int col = 32 * blockIdx.y + c;
+  const float* ml = part_ml + (size_t)h * nsplit * 2;
+  const float* po = part_o + (size_t)h * nsplit * HD + col;
+  const int pos = st->pos;
+  float2 sm[kMaxSplits / 64];
+#pragma unroll
+  for (int i = 0; i < kMaxSplits / 64; ++i)
+    if (64 * i < nsplit) sm[i] = reinterpret_cast<const float2*>(ml)[min(lane + 64 * i, nsplit - 1)];
+  float pv[kMergeK];
+#pragma unroll
+  for (int k = 0; k < kMergeK; ++k)
+    if (kMergeRows * k < nsplit) pv[k] = po[(size_t)min(r + kMergeRows * k, nsplit - 1) * HD];
+  const int active = min((pos + kChunk) / kChunk, nsplit);  // ceil((pos + 1) / chunk)
+  float mloc = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kMaxSplits / 64; ++i)
+    if (64 * i < nsplit && lane + 64 * i < active) mloc = fmaxf(mloc, sm[i].x);
+  const float M = wave_max(mloc);
+  float lsum = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxSplits / 64; ++i) {
+    const int s = lane + 64 * i;
+    if (64 * i < nsplit && s < active) {
+      const float e = __expf(sm[i].x - M);
+      lsum += e * sm[i].y;
+      if (wv == 0) w[s] = e;
+    }
+  }
+  const float L = wave_sum(lsum);
+  __syncthreads();
+  float o = 0.f;
+#pragma unroll
+  for (int k = 0; k < kMergeK; ++k) {
+    const int s = r + kMergeRows * k;
+    if (kMergeRows * k < nsplit && s < active) o += w[s] * pv[k];
+  }
+  o += __shfl_xor(o, 32);
+  if (lane < 32) red[wv][c] = o;
+  __syncthreads();
+  if (tid < 32) out[(size_t)h * HD + col] = (red[0][c] + red[1][c] + red[2][c] + red[3][c]) / L;
 }
 
 // Batched merge: block (h, b) merges head h of sequence b into the activation
@@ -496,7 +560,12 @@ static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const Decod
   else
     launch_k(k_attn_decode<HD, KT, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv,
              st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0);
-  launch_k(k_attn_merge<HD>, dim3(Hq), dim3(HD), 0, s, kLast, part_o, part_ml, nsplit, st, out);
+  if (nsplit <= kMergePf)
+    launch_k(k_attn_merge_head<HD>, dim3(Hq), dim3(HD), 0, s, kLast, part_o, part_ml, nsplit, st,
+             out);
+  else
+    launch_k(k_attn_merge_cols<HD>, dim3(Hq, HD / 32), dim3(256), 0, s, kLast, part_o, part_ml,
+             nsplit, st, out);
   return hipGetLastError();
 }
 
