@@ -222,18 +222,23 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
 // again as three bf16 terms); the values go through LDS transposed to
 // [dimension][position] for the B operand.  Each wavefront keeps its own
 // (max, sum) per head; one barrier, then the four are combined and the split's
-// unnormalised output and statistics written as by k_attn_decode.
+// unnormalised output and statistics written as by k_attn_decode.  Up to G = 5
+// the registers are held to 96 per lane, so five workgroups share a CU (the LDS
+// allows five): a long context's grid (8 KV heads x 129 splits at 8.2K
+// positions) then fits the chip in one round instead of leaving a tail.
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 
 template <int HD, int G>
-__global__ __launch_bounds__(256) void k_attn_decode_mfma(const float* __restrict__ q_in,
-                                                          KvLayout kv,
-                                                          const DecodeState* __restrict__ st,
-                                                          float* __restrict__ part_o,
-                                                          float* __restrict__ part_ml,
-                                                          const SeqDesc* __restrict__ seqs,
-                                                          int layer, int q_stride) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G <= 5 ? 5 : 1))) void
+k_attn_decode_mfma(const float* __restrict__ q_in,
+                   KvLayout kv,
+                   const DecodeState* __restrict__ st,
+                   float* __restrict__ part_o,
+                   float* __restrict__ part_ml,
+                   const SeqDesc* __restrict__ seqs,
+                   int layer,
+                   int q_stride) {
   static_assert(G <= 16, "query heads are the 16 columns of a tile");
   if (seqs) {
     const SeqDesc sd = seqs[blockIdx.z];
