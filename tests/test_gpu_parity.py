@@ -96,12 +96,14 @@ def test_ragged_prompts_chunks_and_pages(cuda_ok, P, chunk, page):
     assert rep.strict_ids, rep.summary()
 
 
-@pytest.mark.parametrize("P,max_seq,page", [(2100, 2200, 16), (2600, 4096, 64),
+@pytest.mark.parametrize("P,max_seq,page", [(2030, 2048, 16), (2060, 2112, 16),
+                                              (2100, 2200, 16), (2600, 4096, 64),
                                               (3000, 9000, 16), (5000, 16384, 128)])
 def test_long_capacity_decode_attention(cuda_ok, P, max_seq, page):
-    """Capacities above 2048 positions give each decode-attention block several
-    64-position sub-chunks (2, 2, 5 and 8 here) under one online softmax, and the
-    merge fewer, longer splits."""
+    """The decode attention grid has one 64-position split per 64 positions of
+    capacity.  Up to 32 splits one workgroup per query head merges them; beyond
+    that, column-sliced workgroups do.  The cases give 32 and 33 splits (either
+    side of that switch), then 35, 64, 141 and 256, the most a launch accepts."""
     cfg = SMALL["gqa128_bf16"]
     prompt = inputs.make_prompt(cfg, P)
     rep, _, _ = run_parity(cfg, prompt, 12, gain_std=0.1, kv_page=page, max_seq=max_seq)
