@@ -81,7 +81,7 @@ typedef struct {
   int32_t tied_embeddings;/* 1: the LM head is the embedding matrix */
   int32_t weight_dtype;   /* wici_dtype of every matrix (norm gains are always F32) */
   int32_t kv_dtype;       /* wici_dtype of the KV cache storage */
-  int32_t max_seq;        /* capacity in positions (prompt + generated) */
+  int32_t max_seq;        /* capacity in positions (prompt + generated); 1..16384 */
   int32_t prefill_chunk;  /* prompt rows processed per pass; 1..8192 */
   int32_t kv_page;        /* positions per KV page: 16, 32, 64 or 128 */
   int32_t prefill_mode;   /* wici_prefill_mode; F32 is required when weight_dtype is F32 */

@@ -46,7 +46,8 @@ def test_memory_requirements_cover_the_weights(name):
 @pytest.mark.parametrize("field,value", [
     ("head_dim", 96), ("d_model", 100), ("ffn_dim", 96 + 1), ("n_kv_heads", 3),
     ("n_layers", 0), ("vocab", 0), ("kv_page", 48), ("prefill_chunk", 0),
-    ("max_seq", 0), ("rms_eps", 0.0), ("rope_base", 1.0), ("prefill_mode", 7),
+    ("max_seq", 0), ("max_seq", 16385), ("rms_eps", 0.0), ("rope_base", 1.0),
+    ("prefill_mode", 7),
     ("flags", 8), ("weight_dtype", 5), ("tied_embeddings", 2)])
 def test_invalid_config_is_rejected(field, value):
     lib = binding.load_library()
