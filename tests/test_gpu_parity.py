@@ -111,6 +111,20 @@ def test_long_capacity_decode_attention(cuda_ok, P, max_seq, page):
     assert rep.strict_ids, rep.summary()
 
 
+@pytest.mark.parametrize("name,P,max_seq,page", [("gqa64_bf16", 2060, 2112, 16),
+                                                   ("gqa64_bf16", 3000, 9000, 16),
+                                                   ("mha64_f32", 2100, 2200, 16)])
+def test_long_capacity_decode_attention_head_dim_64(cuda_ok, name, P, max_seq, page):
+    """Past 32 splits at head dimension 64: each query head's merge takes two
+    32-column workgroups.  The bf16 cache runs on the matrix-core attention
+    kernel (33 and 141 splits), the fp32 cache on the vector one (35 splits)."""
+    cfg = SMALL[name]
+    prompt = inputs.make_prompt(cfg, P)
+    rep, _, _ = run_parity(cfg, prompt, 12, gain_std=0.1, kv_page=page, max_seq=max_seq)
+    assert rep.max_rel_err <= tol_for(cfg)
+    assert rep.strict_ids, rep.summary()
+
+
 @pytest.mark.parametrize("mode", ["bf16x3", "bf16x2", "bf16", "f32"])
 def test_prefill_modes(cuda_ok, mode):
     cfg = SMALL["gqa64_bf16"]
