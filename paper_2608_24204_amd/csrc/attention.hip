@@ -266,7 +266,10 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
   const bf16_t* base = static_cast<const bf16_t*>(kv.base);
   const size_t head_stride = (size_t)kv.page * HD;
 
-  // round trip 1: this lane's page, its query slice (head r16), the position
+  // this lane's page, its query slice (head r16) and the position.  The compiler
+  // tests the position (the exit below) before it issues the page and query
+  // loads, so those follow in a round trip of their own; a fence that keeps them
+  // ahead of the test (two round trips instead of three) measured slower.
   const int jl = start + 16 * wave + r16;  // this lane's key/value position
   const int jc = min(jl, kv.max_pos - 1);
   const int phys = kv.table[jc >> ps];
@@ -284,7 +287,7 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
   const int n = st->pos + 1;
   if (start >= n) return;
 
-  // round trip 2: the keys and values of this lane's position
+  // then the keys and values of this lane's position
   const bf16_t* pk = base + (((size_t)phys * 2 + 0) * Hkv + g) * head_stride +
                      (size_t)(jc & (kv.page - 1)) * HD + 8 * g4;
   const bf16_t* pv = pk + (size_t)Hkv * head_stride;
