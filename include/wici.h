@@ -26,8 +26,9 @@
  *    server thread, as in the paper's context management, Sec. "WiCi Library").
  *  - Device memory is owned by the caller (see wici_bind_memory); the library
  *    owns only host state, captured decode graphs (the per-token step, and the
- *    batched step per batch size it led) and a 16-byte pinned host staging
- *    buffer, all released by wici_destroy.
+ *    batched step per batch size it led) and a 16-byte pinned, device-mapped
+ *    host buffer into which each step's last kernel writes the step state (read
+ *    by the host after the stream drains), all released by wici_destroy.
  */
 #ifndef WICI_H
 #define WICI_H
