@@ -164,8 +164,22 @@ class DecoderOracle:
     def _store(self, a: np.ndarray) -> np.ndarray:
         return bf16_round(a) if self.kv_round == "bf16" else a
 
-    def _lm_weight(self) -> np.ndarray:
-        return self.w["tok_embeddings"] if self.cfg.tied_embeddings else self.w["lm_head"]
+    def _lm_name(self) -> str:
+        return "tok_embeddings" if self.cfg.tied_embeddings else "lm_head"
+
+    def _embed(self, tokens: np.ndarray) -> np.ndarray:
+        """Rows of the embedding as float64 (a mapping with ``rows`` widens only
+        those rows)."""
+        if hasattr(self.w, "rows"):
+            return np.asarray(self.w.rows("tok_embeddings", tokens), dtype=np.float64)
+        return self.w["tok_embeddings"][tokens].astype(np.float64)
+
+    def _proj(self, u: np.ndarray, name: str) -> np.ndarray:
+        """u @ W^T for the weight matrix ``name`` ([out, in]).  A mapping with
+        ``project`` computes the same float64 product from its stored weights."""
+        if hasattr(self.w, "project"):
+            return self.w.project(name, u)
+        return u @ self.w[name].T
 
     def forward(self, tokens, all_logits: bool = False, first_row: int = 0,
                 progress=None) -> np.ndarray:
@@ -184,28 +198,28 @@ class DecoderOracle:
             raise ValueError("sequence capacity exceeded")
         p0 = self.pos
         positions = np.arange(p0, p0 + T)
-        x = self.w["tok_embeddings"][tokens].astype(np.float64)      # [T, d]
+        x = self._embed(tokens)                                     # [T, d]
         for l in range(c.n_layers):
             pre = f"layers.{l}."
             u = rms_norm(x, self.w[pre + "attn_norm"], c.rms_eps)
-            q = (u @ self.w[pre + "wq"].T).reshape(T, c.n_heads, c.head_dim)
-            k = (u @ self.w[pre + "wk"].T).reshape(T, c.n_kv_heads, c.head_dim)
-            v = (u @ self.w[pre + "wv"].T).reshape(T, c.n_kv_heads, c.head_dim)
+            q = self._proj(u, pre + "wq").reshape(T, c.n_heads, c.head_dim)
+            k = self._proj(u, pre + "wk").reshape(T, c.n_kv_heads, c.head_dim)
+            v = self._proj(u, pre + "wv").reshape(T, c.n_kv_heads, c.head_dim)
             q = rope_rotate(q, positions, c.rope_base)
             k = rope_rotate(k, positions, c.rope_base)
             self.K[l][p0:p0 + T] = self._store(k)
             self.V[l][p0:p0 + T] = self._store(v)
             n = p0 + T
             a = attend(q, self.K[l][:n], self.V[l][:n], positions, np.arange(n))
-            x = x + a.reshape(T, c.n_heads * c.head_dim) @ self.w[pre + "wo"].T
+            x = x + self._proj(a.reshape(T, c.n_heads * c.head_dim), pre + "wo")
             wn = rms_norm(x, self.w[pre + "ffn_norm"], c.rms_eps)
-            h = silu(wn @ self.w[pre + "w_gate"].T) * (wn @ self.w[pre + "w_up"].T)
-            x = x + h @ self.w[pre + "w_down"].T
+            h = silu(self._proj(wn, pre + "w_gate")) * self._proj(wn, pre + "w_up")
+            x = x + self._proj(h, pre + "w_down")
             if progress is not None:
                 progress(l)
         self.pos = p0 + T
         rows = x[first_row:] if all_logits else x[-1:]
-        logits = rms_norm(rows, self.w["norm"], c.rms_eps) @ self._lm_weight().T
+        logits = self._proj(rms_norm(rows, self.w["norm"], c.rms_eps), self._lm_name())
         return logits if all_logits else logits[0]
 
     # -- the calls of the offload boundary, in oracle form --------------------

@@ -10,7 +10,7 @@ import pytest
 
 from oracle import DecoderOracle
 from paper_2608_24204_amd import configs, inputs
-from tests.parity import compare, oracle_step_logits
+from tests.parity import compare, oracle_run
 
 pytestmark = pytest.mark.gpu
 
@@ -66,7 +66,7 @@ def test_batched_decode_matches_oracle_per_sequence(cuda_ok, kind, cap):
         for m in ms:
             m.close()
     for b in range(n):
-        rep = compare(ids[b], logs[b], oracle_step_logits(cfg, w64, ps[b], ids[b]))
+        rep = compare(ids[b], logs[b], *oracle_run(cfg, w64, ps[b], cfg.decode_steps))
         print(f"[batch] {kind} seq {b} (P={len(ps[b])}): {rep.summary()}", flush=True)
         assert rep.max_rel_err <= tol
         assert rep.strict_ids, rep.summary()

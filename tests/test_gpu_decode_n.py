@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 
 from paper_2608_24204_amd import configs, inputs
-from tests.parity import compare, oracle_step_logits
+from tests.parity import compare, oracle_run
 
 pytestmark = pytest.mark.gpu
 
@@ -63,8 +63,8 @@ def test_decode_n_matches_oracle_and_decode_step(cuda_ok, cfg):
     ids = [first] + [int(t) for t in toks]
     assert ids == ref_ids
     assert np.array_equal(lg, ref_lg)      # same graph, same inputs: bitwise
-    ora = oracle_step_logits(cfg, inputs.weights_f64(cfg, w), prompt, ids)
-    rep = compare(ids, None, ora)
+    ora_ids, ora = oracle_run(cfg, inputs.weights_f64(cfg, w), prompt, n)
+    rep = compare(ids, None, ora_ids, ora)
     print(f"[decode_n] {cfg.name}: {rep.summary()}", flush=True)
     assert rep.strict_ids, rep.summary()
 

@@ -1,19 +1,27 @@
-"""Full-size parity: a whole greedy request of a workload configuration (its real
-shapes, prompt length and decode steps, the launch configuration the benchmark
-times) on the GPU, against the float64 oracle's logits at every generated step
-(the oracle runs once over prompt + generated ids with all positions' logits, so
-each step is teacher-forced on the GPU's own ids).
+"""Full-size parity: a whole greedy request of each workload configuration (its
+real shapes, prompt length and decode steps, in the launch configuration the
+benchmark times) on the GPU, against the float64 oracle's own greedy run of the
+same request.
 
-The 1B- and 8B-shaped configurations run by default, with bf16 weights and with
-block-scaled 8-bit weights (the oracle then runs on its own quantisation of the
-same bf16 weights); the long-context 8B and the 32B shapes (minutes of float64
-host work each) run when WICI_FULL_PARITY=all.
+The oracle's runs are stored in tests/golden/full/<config>.npz, written by
+tests/golden/make_full_reference.py, which calls only the oracle and the seeded
+input generator.  Each file keeps the oracle's ids and, per step, its largest
+logit, its top 8 and 128 fixed sampled logits, plus the whole logit vector at
+the prefill and at the last step.  A full-size float64 run takes minutes to over
+ten minutes of host time (an 8192-token prompt, a 65 GB model).  The test checks
+that the prompt and the weights are the ones the file was made from, then
+compares (tests/parity.py, compare_fixture):
+- strict: every generated id equals the oracle's;
+- logits: at every step, max |g_i - o_i| / max |o_i| <= 2e-2 over the known
+  entries (all of them at the two stored full vectors);
+- wici_decode_n (the same steps device-resident in one call) gives the same ids.
 
-The five workload configurations of the method must meet the strict criterion
-(every greedy id equal to the oracle's).  The 8-bit variants are held to the
-adjudicated one: any divergent step must be a near tie, the oracle's margin
-between the two tokens within twice that step's largest logit error (both
-verdicts are recorded)."""
+Every configuration is held to the strict criterion except those listed in
+NEAR_TIE: there the oracle's own margin at the named step is below what the
+GPU's float32 arithmetic can resolve, so the test requires that the first
+divergence is at that step and is a near tie by the two-token rule.  It
+compares every step up to that one and prints the verdict as adjudicated.
+"""
 
 from __future__ import annotations
 
@@ -24,16 +32,16 @@ import time
 import numpy as np
 import pytest
 
-from oracle import DecoderOracle
 from paper_2608_24204_amd import configs, inputs
-from tests.parity import LazyQ8F64, compare
+from tests.parity import compare_fixture, load_fixture
 
 pytestmark = pytest.mark.gpu
 
-DEFAULT = ["1b", "8b", "1b_q8", "8b_q8"]
-OPT_IN = ["8b_long", "32b", "32b_q8"]
-SELECTED = DEFAULT + (OPT_IN if os.environ.get("WICI_FULL_PARITY") == "all" else [])
-MODES = os.environ.get("WICI_FULL_PARITY_MODES", "bf16x3").split(",")
+NAMES = ["1b", "8b", "8b_long", "32b", "1b_q8", "8b_q8", "32b_q8"]
+# configuration -> the step of its recorded near tie (the oracle's top-two margin
+# at that step is smaller than the error float32 accumulation order leaves)
+NEAR_TIE: dict[str, int] = {}
+TOL = 2e-2
 
 
 def _report_path():
@@ -42,19 +50,29 @@ def _report_path():
     return os.path.join(d, "full_parity.jsonl")
 
 
-@pytest.mark.parametrize("mode", MODES)
-@pytest.mark.parametrize("name", DEFAULT + OPT_IN)
-def test_full_size_greedy_run_matches_oracle(cuda_ok, name, mode):
-    if name not in SELECTED:
-        pytest.skip("long float64 oracle run; set WICI_FULL_PARITY=all")
+def _digests_match(fx, cfg, w, prompt):
+    from tests.golden.make_full_reference import prompt_digest, weight_digest
+    meta = fx["meta"]
+    assert meta["config"] == cfg.name and meta["decode_steps"] == cfg.decode_steps
+    assert meta["prompt_sha256"] == prompt_digest(prompt), "prompt differs from the stored run's"
+    assert meta["weights_sha256"] == weight_digest(w), "weights differ from the stored run's"
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_full_size_greedy_run_matches_oracle(cuda_ok, name):
     from paper_2608_24204_amd.binding import WiciModel
     cfg = configs.CONFIGS[name]
+    fx = load_fixture(name)
     t0 = time.time()
     w = inputs.make_weights(cfg)
     prompt = inputs.make_prompt(cfg)
-    m = WiciModel(cfg, prefill_mode=mode)
+    _digests_match(fx, cfg, w, prompt)
+    print(f"[full parity] {name}: inputs ready ({time.time() - t0:.1f} s)", flush=True)
+    m = WiciModel(cfg)
     try:
         m.load_weights(w)
+        del w
+        print(f"[full parity] {name}: weights loaded ({time.time() - t0:.1f} s)", flush=True)
         ids, logs = m.generate(prompt, cfg.decode_steps, want_logits=True)
         # the same request with the decode steps run device-resident in one call
         m.reset_kv()
@@ -63,26 +81,16 @@ def test_full_size_greedy_run_matches_oracle(cuda_ok, name, mode):
         ids_n = [first] + [int(t) for t in toks]
     finally:
         m.close()
-    t1 = time.time()
-    seq = np.concatenate([prompt, np.asarray(ids[:-1])])
-    w64 = LazyQ8F64(w) if cfg.weight_dtype == "q8" else inputs.LazyF64(w)
-    orc = DecoderOracle(cfg, w64, max_seq=len(seq))
-    print(f"[full parity] {name}: GPU run done in {t1 - t0:.1f} s; oracle over {len(seq)} "
-          f"positions", flush=True)
-    ora = orc.forward(seq, all_logits=True, first_row=len(prompt) - 1,
-                      progress=lambda l: print(f"[full parity] {name}: oracle layer {l + 1}/"
-                                               f"{cfg.n_layers} ({time.time() - t1:.0f} s)",
-                                               flush=True))
-    t2 = time.time()
-    rep = compare(ids, logs, ora)
-    rec = {"config": name, "prefill_mode": mode, **rep.summary(),
-           "near_tie_steps": rep.near_ties[:10], "gpu_s": t1 - t0, "oracle_s": t2 - t1}
+    rep = compare_fixture(ids, logs, fx)
+    verdict = "strict" if rep.strict_ids else ("adjudicated" if rep.adjudicated else "failed")
+    rec = {"config": name, "verdict": verdict, **rep.summary(),
+           "near_tie_steps": rep.near_ties, "gpu_s": round(time.time() - t0, 1)}
     print("[full parity]", json.dumps(rec), flush=True)
     with open(_report_path(), "a") as f:
         f.write(json.dumps(rec) + "\n")
-    assert rep.max_rel_err <= 2e-2, rec
-    if cfg.weight_dtype == "q8":
-        assert rep.adjudicated, rec
+    assert rep.max_rel_err <= TOL, rec
+    if name in NEAR_TIE:
+        assert rep.strict_ids or (rep.first_divergence == NEAR_TIE[name] and rep.adjudicated), rec
     else:
         assert rep.strict_ids, rec
     assert ids_n == [int(i) for i in ids], "wici_decode_n differs from wici_decode_step"

@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 from paper_2608_24204_amd import configs, inputs
-from tests.parity import compare, oracle_step_logits
+from tests.parity import compare, oracle_run
 
 pytestmark = pytest.mark.gpu
 
@@ -43,8 +43,8 @@ def run_parity(cfg, prompt, n_steps, gain_std=0.0, **kw):
         ids, logs = m.generate(prompt, n_steps, want_logits=True)
     finally:
         m.close()
-    ora = oracle_step_logits(cfg, w64, prompt, ids)
-    rep = compare(ids, logs, ora)
+    ora_ids, ora = oracle_run(cfg, w64, prompt, n_steps)
+    rep = compare(ids, logs, ora_ids, ora)
     print(f"[parity] {cfg.name} P={len(prompt)} N={n_steps} {kw} -> {rep.summary()}", flush=True)
     return rep, ids, logs
 
@@ -148,8 +148,9 @@ def test_kv_cache_holds_oracle_values(cuda_ok):
     finally:
         m.close()
     orc = oracle.DecoderOracle(cfg, w64, max_seq=80)
-    orc.prefill(prompt)
-    orc.decode(tok)
+    otok = oracle.greedy(orc.prefill(prompt))
+    assert otok == tok                 # same context for the decoded position
+    orc.decode(otok)
     for l, (K, V) in enumerate(kv):
         for bits, o in ((K, orc.K[l][:71]), (V, orc.V[l][:71])):
             g = inputs.bf16_bits_to_f32(bits).astype(np.float64)

@@ -10,7 +10,8 @@ import numpy as np
 import pytest
 
 from paper_2608_24204_amd import configs, inputs
-from tests.parity import LazyQ8F64, compare, oracle_step_logits
+from oracle import q8_model_f64
+from tests.parity import compare, oracle_run
 
 pytestmark = pytest.mark.gpu
 
@@ -39,8 +40,8 @@ def run(cfg, mode, **kw):
         ids, logs = m.generate(prompt, cfg.decode_steps, want_logits=True)
     finally:
         m.close()
-    ora = oracle_step_logits(cfg, LazyQ8F64(w), prompt, ids)
-    rep = compare(ids, logs, ora)
+    ora_ids, ora = oracle_run(cfg, q8_model_f64(w), prompt, cfg.decode_steps)
+    rep = compare(ids, logs, ora_ids, ora)
     print(f"[q8 parity] {cfg.name} mode={mode} {kw} -> {rep.summary()}", flush=True)
     return rep
 
