@@ -154,7 +154,10 @@ wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
  * previous prefill/decode call returned) at the current position and return the
  * next token (and optionally the logits, as for wici_prefill).  Synchronous.
  * Errors: WICI_E_ARG (NULL next_token, token_in >= vocab), WICI_E_STATE (no
- * prefill since the last reset), WICI_E_CAPACITY, WICI_E_NUMERIC. */
+ * prefill since the last reset), WICI_E_CAPACITY, WICI_E_NUMERIC, WICI_E_HIP
+ * (also when the attention kernel finds that the blocks of one KV head, which
+ * exchange their partial results through one XCD's L2 cache, did not all run
+ * on the same XCD: the step's results are then not trusted; sticky). */
 wici_status wici_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
                              float* logits);
 
@@ -201,7 +204,8 @@ wici_status wici_bind_memory_shared(wici_model* m, const wici_model* src, void* 
  * as token_in of wici_decode_step; next_tokens (host, n) receives each next
  * token; logits (host, n * vocab, may be NULL) each sequence's fp32 logits,
  * row b for sequence b.  Runs on models[0]'s stream and scratch (n <= its prefill_chunk and
- * <= 256).  Synchronous.  Errors: WICI_E_ARG (bad pointers or counts, models
+ * <= 256); n == 1 runs models[0]'s own decode step (wici_decode_step), whose
+ * weight-streaming products are faster for a single row.  Synchronous.  Errors: WICI_E_ARG (bad pointers or counts, models
  * that do not share weights and configuration, duplicates, a token id >= vocab,
  * n beyond the scratch), WICI_E_STATE (a model not ready, not prefilled or
  * without a token to feed), WICI_E_CAPACITY (a model at max_seq),
@@ -229,11 +233,13 @@ wici_status wici_read_kv(wici_model* m, int32_t layer, int32_t begin, int32_t en
  * its kernels' dispatches record as the first kernel starts and the last one
  * ends (kernel execution time, without the gaps between launches).  Writes the
  * duration in ms of each launch, in launch order, to durations_ms (capacity
- * entries) and their number (3 + 5 * n_layers) to *n_written.  Order: embedding;
- * per layer: QKV GEMV (with RoPE and the KV append), attention (split pass
- * start to merge end), O GEMV, gate/up GEMV, down GEMV; then the LM head GEMV
- * and the final argmax.  Errors as wici_decode_step, plus WICI_E_ARG for NULL
- * outputs or a capacity below 3 + 5 * n_layers. */
+ * entries) and their number (3 + 5 * n_layers) to *n_written.  Order: embedding
+ * (0 with bf16 weights, whose first QKV GEMV gathers the embedding row itself);
+ * per layer: QKV GEMV (with RoPE and the KV append), attention (with a bf16
+ * cache and at most 32 splits one launch that also merges the splits, else
+ * split pass start to merge end), O GEMV, gate/up GEMV, down GEMV; then the LM
+ * head GEMV and the final argmax.  Errors as wici_decode_step, plus WICI_E_ARG
+ * for NULL outputs or a capacity below 3 + 5 * n_layers. */
 wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
                                      float* durations_ms, int32_t capacity, int32_t* n_written);
 
@@ -279,12 +285,33 @@ enum {
  * outcome[i] receives one WICI_CACHE_* value per tensor.  Uploading follows
  * wici_load_weights (same names, shapes, dtypes, errors).  Errors: WICI_E_ARG
  * (NULL model/store_dir/outcome, a negative threshold, a bad shape, data NULL
- * where it is needed), anything wici_load_weights returns; a store file that
- * cannot be written is not an error. */
+ * where it is needed, a tensor given with both a hash and data that misses the
+ * store and whose data does not have that hash: it would be saved under the
+ * wrong name; checked before anything is uploaded), anything wici_load_weights
+ * returns; a store file that cannot be written is not an error. */
 wici_status wici_load_weights_cached(wici_model* m, const wici_tensor* tensors,
                                      const uint8_t* hashes, int32_t n_tensors,
                                      const char* store_dir, int64_t threshold_bytes,
                                      int32_t* outcome);
+
+/* Diagnostic, no model: the plain streaming-read rate of device memory, the
+ * ceiling a weight-streaming decode step is held to (the paper's per-token work
+ * is bound by reading the model's weights, Sec. "Batching and Trace Replay").
+ * d_buf: device buffer of `bytes` bytes (a multiple of 16384), read whole `reps`
+ * times by `grid` 256-thread workgroups, workgroup b reading the 16 KiB blocks
+ * b, b + grid, ... with four non-temporal 16-byte loads per lane in flight.
+ * d_sink: device workspace of 256 * grid + 1 32-bit words: word 256 b + t
+ * receives the XOR of the words thread t of workgroup b read, word 256 * grid
+ * their XOR when a checksum is asked for.  Both buffers stay with the caller.
+ * Runs on hip_stream (NULL: the null stream) and waits for it; *ms_per_read
+ * receives the average time of one read (events around the reads only).
+ * checksum (host, may be NULL) receives the XOR of every 32-bit word of the
+ * buffer (each word is read by exactly one thread, so the result does not
+ * depend on the grid).  Errors: WICI_E_ARG (NULL pointers, sizes), WICI_E_HIP (a
+ * HIP call failed). */
+wici_status wici_stream_read(const void* d_buf, size_t bytes, int32_t grid, int32_t reps,
+                             void* d_sink, void* hip_stream, float* ms_per_read,
+                             uint32_t* checksum);
 
 /* Message of the last failed call on this model ("" if none).  Valid until the
  * next call on the model. */

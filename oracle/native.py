@@ -9,7 +9,7 @@ product's device layout.  It provides three things:
 - ``w.project(name, u)``: the product u @ W^T in float64.  For a few rows of u
   (a decode step) it calls the plain C dot products of ``matvec.c``, which read
   the stored weights directly.  For more rows (a prefill) it widens the matrix
-  and uses numpy's float64 matrix multiply.
+  a block of rows at a time and uses numpy's float64 matrix multiply.
 
 Both routes compute the same float64 products and sums.  Only the order of the
 additions differs, so results agree to rounding (pinned in
@@ -32,6 +32,10 @@ LIB = os.path.join(HERE, "_lib", "liboracle_matvec.so")
 # at most this many rows of u take the C dot products; more rows go to the
 # widened matrix multiply (compute-bound work that BLAS does better)
 C_MAX_ROWS = 16
+# the widened multiply takes the weights this many elements at a time (whole
+# rows): small temporaries are reused by the allocator, where widening a whole
+# matrix at once spends most of its time faulting in fresh pages
+WIDEN_BLOCK = 1 << 21
 
 _lock = threading.Lock()
 _lib = None
@@ -118,5 +122,10 @@ class StoredWeights:
     def project(self, name: str, u: np.ndarray) -> np.ndarray:
         w = self._w[name]
         if u.ndim == 2 and u.shape[0] > C_MAX_ROWS:
-            return u @ widen(w).T
+            N, K = w.shape
+            y = np.empty((u.shape[0], N))
+            step = max(1, WIDEN_BLOCK // max(K, 1))
+            for r in range(0, N, step):
+                y[:, r:r + step] = u @ widen(w[r:r + step]).T
+            return y
         return matvec(w, u)

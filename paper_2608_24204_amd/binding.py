@@ -30,7 +30,7 @@ EXPORTED = ["wici_create", "wici_memory_requirements", "wici_bind_memory", "wici
             "wici_prefill", "wici_decode_step", "wici_decode_n", "wici_reset_kv", "wici_position",
             "wici_read_kv", "wici_profile_decode_step", "wici_quantize_q8", "wici_md5",
             "wici_load_weights_cached", "wici_bind_memory_shared", "wici_decode_batch",
-            "wici_last_error", "wici_destroy"]
+            "wici_stream_read", "wici_last_error", "wici_destroy"]
 
 
 class WiciConfig(ctypes.Structure):
@@ -91,6 +91,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
                                       ctypes.c_int64, P], ctypes.c_int),
         "wici_bind_memory_shared": ([P, P, P, sz, P, sz], ctypes.c_int),
         "wici_decode_batch": ([P, i32, P, P, P], ctypes.c_int),
+        "wici_stream_read": ([P, sz, i32, i32, P, P, ctypes.POINTER(ctypes.c_float), P],
+                             ctypes.c_int),
         "wici_last_error": ([P], ctypes.c_char_p),
         "wici_destroy": ([P], None),
     }
@@ -152,6 +154,27 @@ def md5(data) -> bytes:
     if st != WICI_OK:
         raise WiciError(st, "wici_md5")
     return bytes(out)
+
+
+def stream_read(buf, grid: int, reps: int, sink, stream=None, checksum: bool = False):
+    """One plain streaming read of the device tensor ``buf`` by ``grid`` workgroups,
+    ``reps`` times (wici_stream_read): returns the average ms per read, and with
+    ``checksum`` also the XOR of the buffer's 32-bit words.  ``sink`` is a device
+    tensor of at least 4 * (256 * grid + 1) bytes; ``stream`` a torch stream
+    (default: the current one)."""
+    import torch
+    lib = load_library()
+    st = (stream or torch.cuda.current_stream()).cuda_stream
+    if sink.numel() * sink.element_size() < 4 * (256 * grid + 1):
+        raise ValueError("sink too small")
+    ms = ctypes.c_float()
+    ck = ctypes.c_uint32()
+    r = lib.wici_stream_read(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
+                             grid, reps, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(st),
+                             ctypes.byref(ms), ctypes.byref(ck) if checksum else None)
+    if r != WICI_OK:
+        raise WiciError(r, "wici_stream_read failed")
+    return (float(ms.value), int(ck.value)) if checksum else float(ms.value)
 
 
 def memory_requirements(c: WiciConfig) -> tuple[int, int, int]:

@@ -228,9 +228,131 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
 // positions) then fits the chip in one round instead of leaving a tail.
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// Merge of a KV head's splits in the last of its split blocks to finish (the
+// batch-1 launch of k_attn_decode_mfma with FUSE, at most kFuseMaxSplits splits).
+// Every split of head g runs on the same XCD, so the blocks exchange their
+// partials through that XCD's L2 alone: each block's stores are acknowledged by
+// the L2 (a wait for all of them) before it takes a ticket from the head's
+// counter, an atomic performed in the same L2.  The block drawing the last
+// ticket reads the partials with loads that bypass its CU's L1 (another
+// workgroup on the CU may hold an older copy of a line) and merges them:
+// out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s.  It then resets
+// the counter for the next launch.  The placement is checked, not assumed: each
+// block records the XCD it ran on (the hardware's XCC id) and the merging block
+// compares them with its own; a mismatch sets fz.state->fault, which the step
+// reports as an error.
+constexpr int kFuseMaxSplits = 32;
+constexpr int kFuseLine = 64;   // ints per head of the counter and XCD arrays (256 bytes)
+
+__device__ __forceinline__ int xcc_id() {
+  return (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 0xf);
+}
+
+// 16 bytes at byte offset `off` of the buffer `r`, read past the L1 (sc0).
+__device__ __forceinline__ u32x4_t load_l2(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 1);
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
+}
 
 template <int HD, int G>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G <= 5 ? 5 : 1))) void
+__device__ __forceinline__ void attn_merge_in_last_split(const AttnFuse& fz, int g, int split,
+                                                         int nsplit, int n,
+                                                         const float* part_o,
+                                                         const float* part_ml) {
+  constexpr int COLS = G * HD / 4;      // float4 columns of the group's output
+  constexpr int P = 256 / COLS;         // threads per column (>= 2)
+  constexpr int PER = kFuseMaxSplits / P;
+  __shared__ int s_last;
+  __shared__ float s_w[G][kFuseMaxSplits];
+  __shared__ float4 s_red[P][COLS];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int active = (n + kChunk - 1) / kChunk;
+  const int me = xcc_id();
+  if (tid == 0) fz.xcc[g * kFuseLine + split] = me;
+  // this thread's stores have reached the L2 (the empty asm keeps the compiler
+  // from moving memory operations across the wait)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0);
+  asm volatile("" ::: "memory");
+  __syncthreads();
+  if (tid == 0) {
+    const int old = __hip_atomic_fetch_add(fz.cnt + g * kFuseLine, 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+    s_last = old == active - 1;
+    if (old == active - 1)
+      __hip_atomic_store(fz.cnt + g * kFuseLine, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  __syncthreads();
+  if (!s_last) return;
+
+  // the group's partials: column c of splits p, p + P, ... (clamped, all issued at once)
+  const int c = tid % COLS, p = tid / COLS;
+  const int hl = c / (HD / 4), d4 = c % (HD / 4);
+  const int hh = g * G + hl;
+  const __amdgpu_buffer_rsrc_t ro = rsrc(part_o, (size_t)fz.n_heads * nsplit * HD * 4);
+  const __amdgpu_buffer_rsrc_t rm = rsrc(part_ml, (size_t)fz.n_heads * nsplit * 2 * 4);
+  const __amdgpu_buffer_rsrc_t rx = rsrc(fz.xcc, (size_t)fz.n_kv * kFuseLine * 4);
+  u32x4_t pv[PER];
+  if (p < P) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int sp = min(p + P * k, active - 1);
+      pv[k] = load_l2(ro, (int)((((size_t)hh * nsplit + sp) * HD + 4 * d4) * 4));
+    }
+  }
+  // statistics: one wavefront per head, lane = split
+  for (int h = wave; h < G; h += 4) {
+    const int hq = g * G + h, sp = min(lane, active - 1);
+    const size_t f = ((size_t)hq * nsplit + sp) * 2;   // float index of (m, l)
+    const u32x4_t st2 = load_l2(rm, (int)((f & ~(size_t)3) * 4));
+    const u32x4_t xv = load_l2(rx, (g * kFuseLine + (sp & ~3)) * 4);
+    // both loads in one round trip (the compiler would otherwise issue the XCD
+    // record's load only inside the branch that tests it, after the reductions)
+    asm volatile("" ::"v"(st2.x), "v"(xv.x));
+    const bool odd = (f & 3) != 0;
+    const float mv = __uint_as_float(odd ? st2.z : st2.x), lv = __uint_as_float(odd ? st2.w : st2.y);
+    const int xo = (int)(xv[sp & 3]);
+    const bool on = lane < active;
+    const float M = wave_max(on ? mv : -INFINITY);
+    const float e = on ? __expf(mv - M) : 0.f;
+    const float L = wave_sum(e * (on ? lv : 0.f));
+    if (on) s_w[h][lane] = e / L;
+    if (on && xo != me) static_cast<DecodeState*>(fz.state)->fault = 1;
+  }
+  __syncthreads();
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (p < P) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int sp = p + P * k;
+      if (sp < active) {
+        const float w = s_w[hl][sp];
+        acc.x += w * __uint_as_float(pv[k].x);
+        acc.y += w * __uint_as_float(pv[k].y);
+        acc.z += w * __uint_as_float(pv[k].z);
+        acc.w += w * __uint_as_float(pv[k].w);
+      }
+    }
+    s_red[p][c] = acc;
+  }
+  __syncthreads();
+  if (tid < COLS) {
+    float4 o = s_red[0][tid];
+#pragma unroll
+    for (int q = 1; q < P; ++q) {
+      const float4 t = s_red[q][tid];
+      o.x += t.x; o.y += t.y; o.z += t.z; o.w += t.w;
+    }
+    reinterpret_cast<float4*>(fz.out)[(size_t)g * COLS + tid] = o;
+  }
+}
+
+template <int HD, int G, bool FUSE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G <= 5 && !FUSE ? 5 : 1))) void
 k_attn_decode_mfma(const float* __restrict__ q_in,
                    KvLayout kv,
                    const DecodeState* __restrict__ st,
@@ -238,8 +360,10 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
                    float* __restrict__ part_ml,
                    const SeqDesc* __restrict__ seqs,
                    int layer,
-                   int q_stride) {
+                   int q_stride,
+                   AttnFuse fz) {
   static_assert(G <= 16, "query heads are the 16 columns of a tile");
+  static_assert(!FUSE || G * HD <= 512, "the merge holds at most 16 partials per thread");
   if (seqs) {
     const SeqDesc sd = seqs[blockIdx.z];
     kv.base = static_cast<char*>(sd.kv) + (size_t)layer * sd.kv_layer_stride;
@@ -257,8 +381,21 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
   __shared__ float wm[4][G], wl[4][G];
   __shared__ float wo[4][G][HD];
 
-  const int nsplit = gridDim.x, split = blockIdx.x, g = blockIdx.y;
   const int Hkv = kv.n_kv;
+  int nsplit, split, g;
+  if constexpr (FUSE) {
+    // 1-D grid dealt to the XCDs in turn: block b runs on XCD b % 8, and every
+    // split of KV head g is placed on XCD g % 8 (blocks of absent heads exit)
+    const int b = blockIdx.x, x = b & 7, r = b >> 3, h8 = (Hkv + 7) >> 3;
+    g = x + 8 * (r % h8);
+    split = r / h8;
+    nsplit = fz.nsplit;
+    if (g >= Hkv) return;
+  } else {
+    nsplit = gridDim.x;
+    split = blockIdx.x;
+    g = blockIdx.y;
+  }
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int start = split * kChunk;
@@ -403,6 +540,7 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
       part_ml[((size_t)hh * nsplit + split) * 2 + 1] = L;
     }
   }
+  if constexpr (FUSE) attn_merge_in_last_split<HD, G>(fz, g, split, nsplit, n, part_o, part_ml);
 }
 
 // out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s over the active
@@ -561,10 +699,24 @@ __global__ __launch_bounds__(HD) void k_attn_merge_batch(const float* __restrict
 template <int HD, typename KT, int G>
 static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const DecodeState* st,
                                 int nsplit, float* part_o, float* part_ml, float* out,
-                                hipStream_t s) {
+                                const AttnFuse* fuse, hipStream_t s) {
+  if constexpr (sizeof(KT) == 2 && G * HD <= 512) {
+    // the merge in the last split block (one launch) when the splits fit it
+    if (fuse && nsplit <= kFuseMaxSplits) {
+      AttnFuse fz = *fuse;
+      fz.out = out;
+      fz.nsplit = nsplit;
+      fz.n_heads = Hq;
+      fz.n_kv = kv.n_kv;
+      const int blocks = 8 * ((kv.n_kv + 7) / 8) * nsplit;
+      launch_k(k_attn_decode_mfma<HD, G, true>, dim3(blocks), dim3(256), 0, s, kOnly, q, kv, st,
+               part_o, part_ml, (const SeqDesc*)nullptr, 0, 0, fz);
+      return hipGetLastError();
+    }
+  }
   if constexpr (sizeof(KT) == 2)
-    launch_k(k_attn_decode_mfma<HD, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv,
-             st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0);
+    launch_k(k_attn_decode_mfma<HD, G, false>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q,
+             kv, st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0, AttnFuse{});
   else
     launch_k(k_attn_decode<HD, KT, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv,
              st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0);
@@ -582,8 +734,9 @@ static hipError_t attn_decode_batch_t(const float* q, int q_stride, int B, int H
                                       const SeqDesc* seqs, int layer, int nsplit, float* part_o,
                                       float* part_ml, const ActBuf& out, hipStream_t s) {
   if constexpr (sizeof(KT) == 2)
-    hipLaunchKernelGGL((k_attn_decode_mfma<HD, G>), dim3(nsplit, kv.n_kv, B), dim3(256), 0, s, q,
-                       kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer, q_stride);
+    hipLaunchKernelGGL((k_attn_decode_mfma<HD, G, false>), dim3(nsplit, kv.n_kv, B), dim3(256), 0,
+                       s, q, kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer,
+                       q_stride, AttnFuse{});
   else
     hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv, B), dim3(256), 0, s, q,
                        kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer, q_stride);
@@ -595,13 +748,13 @@ static hipError_t attn_decode_batch_t(const float* q, int q_stride, int B, int H
 template <int HD, typename KT>
 static hipError_t attn_decode_g(int G, const float* q, int Hq, KvLayout kv,
                                 const DecodeState* st, int nsplit, float* part_o,
-                                float* part_ml, float* out, hipStream_t s) {
+                                float* part_ml, float* out, const AttnFuse* fz, hipStream_t s) {
   switch (G) {
-    case 1: return attn_decode_t<HD, KT, 1>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
-    case 2: return attn_decode_t<HD, KT, 2>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
-    case 4: return attn_decode_t<HD, KT, 4>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
-    case 5: return attn_decode_t<HD, KT, 5>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
-    case 8: return attn_decode_t<HD, KT, 8>(q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    case 1: return attn_decode_t<HD, KT, 1>(q, Hq, kv, st, nsplit, part_o, part_ml, out, fz, s);
+    case 2: return attn_decode_t<HD, KT, 2>(q, Hq, kv, st, nsplit, part_o, part_ml, out, fz, s);
+    case 4: return attn_decode_t<HD, KT, 4>(q, Hq, kv, st, nsplit, part_o, part_ml, out, fz, s);
+    case 5: return attn_decode_t<HD, KT, 5>(q, Hq, kv, st, nsplit, part_o, part_ml, out, fz, s);
+    case 8: return attn_decode_t<HD, KT, 8>(q, Hq, kv, st, nsplit, part_o, part_ml, out, fz, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -644,22 +797,25 @@ bool attn_group_supported(int G) { return G == 1 || G == 2 || G == 4 || G == 5 |
 
 hipError_t launch_attn_decode(bool kv_bf16, const float* q, int Hq, KvLayout kv,
                               const void* state, int nsplit, float* part_o, float* part_ml,
-                              float* out, hipStream_t s) {
+                              float* out, const AttnFuse* fuse, hipStream_t s) {
   if (nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos || kv.n_kv < 1 || Hq % kv.n_kv ||
       kv.page < 1 || (kv.page & (kv.page - 1)))
     return hipErrorInvalidValue;
+  if (fuse && (!fuse->cnt || !fuse->xcc || !fuse->state)) return hipErrorInvalidValue;
   const DecodeState* st = static_cast<const DecodeState*>(state);
   const int G = Hq / kv.n_kv;
   if (kv.hd == 128) {
-    if (kv_bf16) return attn_decode_g<128, bf16_t>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
-    return attn_decode_g<128, float>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    if (kv_bf16) return attn_decode_g<128, bf16_t>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, fuse, s);
+    return attn_decode_g<128, float>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, fuse, s);
   }
   if (kv.hd == 64) {
-    if (kv_bf16) return attn_decode_g<64, bf16_t>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
-    return attn_decode_g<64, float>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, s);
+    if (kv_bf16) return attn_decode_g<64, bf16_t>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, fuse, s);
+    return attn_decode_g<64, float>(G, q, Hq, kv, st, nsplit, part_o, part_ml, out, fuse, s);
   }
   return hipErrorInvalidValue;
 }
+
+int attn_fuse_ints(int n_kv) { return 2 * n_kv * kFuseLine; }
 
 // ------------------------------------------------------------------- prefill
 template <int HD, typename KT>

@@ -178,6 +178,21 @@ extern "C" wici_status wici_load_weights_cached(wici_model* m, const wici_tensor
       outcome[i] = WICI_CACHE_HIT;
       up.push_back(t);
     } else if (t.data) {
+      if (hashes) {
+        // the file will be named by this hash: a given hash must be the data's
+        // own, or the store would serve the wrong tensor for it from then on
+        std::vector<char> host;
+        const void* src = t.data;
+        if (t.on_device) {
+          host.resize(bytes);
+          if (hipMemcpy(host.data(), t.data, bytes, hipMemcpyDeviceToHost) != hipSuccess)
+            return WICI_E_HIP;
+          src = host.data();
+        }
+        uint8_t own[16];
+        wici_md5(src, bytes, own);
+        if (std::memcmp(own, md5, 16) != 0) return WICI_E_ARG;
+      }
       outcome[i] = WICI_CACHE_SAVED;
       to_save.emplace_back(path, (int)up.size());
       up.push_back(t);

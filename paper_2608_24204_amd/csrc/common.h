@@ -136,7 +136,8 @@ struct DecodeState {  // device-resident step state
   int32_t pos;        // number of cached positions
   int32_t token;      // last emitted (or host-given) token
   int32_t bad;        // nonzero: a logit was NaN/Inf in the last argmax
-  int32_t pad;
+  int32_t fault;      // nonzero: a decode attention's split blocks of one KV head ran
+                      // on different XCDs (see AttnFuse); sticky until reset
 };
 
 }  // namespace wici

@@ -103,7 +103,7 @@ __host__ __device__ constexpr int gemv_rows(int epi, int J, bool q8 = false) {
          : (J == 1 ? (q8 ? 8 : 4) : J <= 4 ? 2 : 1);
 }
 
-template <typename WT, int EPI, int J, bool DB>
+template <typename WT, int EPI, int J, bool DB, bool EMB>
 __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, int K,
                                               const float* __restrict__ x,
                                               const float* __restrict__ gain, float eps,
@@ -113,6 +113,10 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
                                               const unsigned short* __restrict__ S) {
   constexpr int R = gemv_rows(EPI, J, sizeof(WT) == 1);
   constexpr bool NORM = EPI != GEMV_RESID;   // the residual GEMVs take x as is
+  // EMB (first layer's QKV projection, bf16 weights): x is the embedding row of
+  // the state's token, gathered here; workgroup 0 also stores it as the residual
+  // stream x (which the caller passes as `x`)
+  static_assert(!EMB || (EPI == GEMV_QKV && sizeof(WT) == 2), "embedding gather: bf16 QKV only");
   constexpr bool Q8 = sizeof(WT) == 1;
   constexpr int EPL = LaneElems<WT>::n, SPAN = 256 * EPL, NF4 = EPL / 4;
   extern __shared__ float ps[];  // [4 wavefronts][max_rows] row-sum shares
@@ -141,13 +145,16 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
   auto kofs = [&](int j) { return min(tid * EPL + j * SPAN, K - EPL); };
 
   // ---- prologue: x, gain and residual loads, then the first group's weights -----
+  // (EMB: the token first, the gain, the weights, then the token's embedding row)
+  int etok = 0;
+  if constexpr (EMB) etok = static_cast<const DecodeState*>(rope.state)->token;
   float4 xv[J][NF4], xg[NORM ? J : 1][NF4];
 #pragma unroll
   for (int j = 0; j < J; ++j)
 #pragma unroll
     for (int q = 0; q < NF4; ++q) {
       const int f = (kofs(j) >> 2) + q;
-      xv[j][q] = reinterpret_cast<const float4*>(x)[f];
+      if (!EMB) xv[j][q] = reinterpret_cast<const float4*>(x)[f];
       if (NORM) xg[NORM ? j : 0][q] = reinterpret_cast<const float4*>(gain)[f];
     }
   float yres = 0.f;  // residual of local row tid
@@ -175,6 +182,24 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
   if (EPI == GEMV_QKV) {
     pos = static_cast<const DecodeState*>(rope.state)->pos;
     phys = rope.kv.table[pos / rope.kv.page];
+  }
+  if constexpr (EMB) {
+    // a negative token (left by a failed step) reads as a zero row
+    const bf16_t* er = static_cast<const bf16_t*>(rope.embed) + (size_t)max(etok, 0) * K;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(er + kofs(j));
+      const bool z = etok < 0;
+      xv[j][0] = make_float4(z ? 0.f : __uint_as_float(v.x << 16), z ? 0.f : __uint_as_float(v.x & 0xffff0000u),
+                             z ? 0.f : __uint_as_float(v.y << 16), z ? 0.f : __uint_as_float(v.y & 0xffff0000u));
+      xv[j][1] = make_float4(z ? 0.f : __uint_as_float(v.z << 16), z ? 0.f : __uint_as_float(v.z & 0xffff0000u),
+                             z ? 0.f : __uint_as_float(v.w << 16), z ? 0.f : __uint_as_float(v.w & 0xffff0000u));
+      if (blk == 0 && tid * EPL + j * SPAN < K) {
+        float4* xo = reinterpret_cast<float4*>(const_cast<float*>(x) + kofs(j));
+        xo[0] = xv[j][0];
+        xo[1] = xv[j][1];
+      }
+    }
   }
 
   // x slices of this lane (times the gain; zero past the row end), their sum of
@@ -376,11 +401,11 @@ static GemvCfg gemv_cfg(int wt, int epi, int N, int K) {
   return c;
 }
 
-template <typename WT, int EPI, int J, bool DB>
+template <typename WT, int EPI, int J, bool DB, bool EMB>
 static hipError_t gemv_go(const GemvCfg& cf, const WT* W, int N, int K, const float* x,
                           const float* gain, float eps, float* y, ArgmaxPart* part,
                           int* nblocks, hipStream_t st, const QkvRope& rp) {
-  if constexpr (sizeof(WT) != 2 && J > 8) {
+  if constexpr ((sizeof(WT) != 2 && J > 8) || (EMB && (EPI != GEMV_QKV || sizeof(WT) != 2))) {
     return hipErrorInvalidValue;
   } else {
     constexpr bool Q8 = sizeof(WT) == 1;
@@ -394,7 +419,7 @@ static hipError_t gemv_go(const GemvCfg& cf, const WT* W, int N, int K, const fl
       int dev = 0, cus = 0, per_cu = 0;
       if (hipGetDevice(&dev) != hipSuccess ||
           hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-          hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_gemv<WT, EPI, J, DB>, 256, 4096) !=
+          hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_gemv<WT, EPI, J, DB, EMB>, 256, 4096) !=
               hipSuccess)
         return 0;
       return cus * per_cu;
@@ -409,13 +434,13 @@ static hipError_t gemv_go(const GemvCfg& cf, const WT* W, int N, int K, const fl
       c.lds = (size_t)4 * c.max_rows * sizeof(float);
     }
     if (nblocks) *nblocks = c.grid;
-    launch_k(k_gemv<WT, EPI, J, DB>, dim3(c.grid), dim3(256), c.lds, st, kOnly, W, N, K, x, gain,
+    launch_k(k_gemv<WT, EPI, J, DB, EMB>, dim3(c.grid), dim3(256), c.lds, st, kOnly, W, N, K, x, gain,
              eps, y, part, c.max_rows, rp, S);
     return hipGetLastError();
   }
 }
 
-template <typename WT, int EPI>
+template <typename WT, int EPI, bool EMB = false>
 static hipError_t gemv_dispatch(const GemvCfg& cf, const WT* W, int N, int K, const float* x,
                                 const float* gain, float eps, float* y, ArgmaxPart* part,
                                 int* nblocks, hipStream_t st, const QkvRope& rp) {
@@ -425,8 +450,8 @@ static hipError_t gemv_dispatch(const GemvCfg& cf, const WT* W, int N, int K, co
 #define WICI_J(JJ)                                                                    \
   case JJ:                                                                            \
     return cf.db && JJ <= kDbMaxJ                                                     \
-               ? gemv_go<WT, EPI, JJ, (JJ <= kDbMaxJ)>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp) \
-               : gemv_go<WT, EPI, JJ, false>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp)
+               ? gemv_go<WT, EPI, JJ, (JJ <= kDbMaxJ), EMB>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp) \
+               : gemv_go<WT, EPI, JJ, false, EMB>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp)
   switch (cf.J) {
     WICI_J(1); WICI_J(2); WICI_J(3); WICI_J(4); WICI_J(5); WICI_J(6); WICI_J(7); WICI_J(8);
     WICI_J(10); WICI_J(12); WICI_J(14); WICI_J(16);
@@ -455,6 +480,12 @@ static hipError_t gemv_t(int epi, const WT* W, int N, int K, const float* x, con
   }
   if (epi == GEMV_SWIGLU && N % 2) return hipErrorInvalidValue;
   const GemvCfg cf = gemv_cfg(wt, epi, N, K);
+  if (epi == GEMV_QKV && rp.embed) {
+    if constexpr (wt == W_BF16)
+      return gemv_dispatch<WT, GEMV_QKV, true>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp);
+    else
+      return hipErrorInvalidValue;
+  }
 #define WICI_GEMV_EPI(E) \
   case E: return gemv_dispatch<WT, E>(cf, W, N, K, x, gain, eps, y, part, nblocks, st, rp)
   switch (epi) {

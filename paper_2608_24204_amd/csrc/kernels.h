@@ -56,6 +56,11 @@ struct QkvRope {
   int kv_bf16;         // cache element type: 1 bf16, 0 fp32
   int n_q;             // query heads
   float q_scale;       // 1/sqrt(hd)
+  // bf16 embedding [V, K] or nullptr.  Set: the projection's input is the
+  // embedding row of the state's token (a negative token gives a zero row)
+  // instead of x, and that row is also stored into x (the residual stream), so
+  // no separate gather runs before the first layer.
+  const void* embed;
 };
 
 // y = W x for W [N, K] row-major (bf16 bits or fp32), x fp32 [K].
@@ -89,6 +94,15 @@ hipError_t launch_embed(int wt, const void* E, int V, int d, const int32_t* toke
 hipError_t launch_set_token(void* state, int token, hipStream_t st);
 hipError_t launch_reset_state(void* state, hipStream_t st);
 hipError_t launch_init_block_table(int32_t* table, int n_pages, hipStream_t st);
+// One plain streaming read of `bytes` (a multiple of 16 KiB) of device memory by
+// `grid` workgroups; sink[256 b + t] receives the XOR of the 32-bit words thread t
+// of workgroup b read (every word of the buffer is read by exactly one thread).
+hipError_t launch_stream_read(const void* buf, size_t bytes, int grid, unsigned* sink,
+                              hipStream_t st);
+// out[0] = XOR of in[0 .. n) (one workgroup).
+hipError_t launch_xor_reduce(const unsigned* in, int n, unsigned* out, hipStream_t st);
+// p[i] = v for i < n (a fill kernel, so it can sit in captured work).
+hipError_t launch_fill_i32(int32_t* p, int n, int v, hipStream_t st);
 
 // y[t, :] = RMSNorm(x[t, :]) * gain for T rows of width d (row stride d).
 hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int T, int d,
@@ -134,14 +148,31 @@ hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
                                KvLayout kv, const ActBuf& out, hipStream_t st);
 
+// The merge of a batch-1 decode attention done by the last split block of each
+// KV head (one launch, no merge kernel), for bf16 caches of up to 32 splits.
+// cnt and xcc each hold 64 ints per KV head (attn_fuse_ints(n_kv) ints in all,
+// cnt first); the counters must be zero before the first launch and are zero
+// again after every launch.  state is the step's DecodeState: its `fault` field
+// is set if the splits of one head did not all run on one XCD (their partials
+// then cannot be trusted).  The launcher fills in the other fields.
+struct AttnFuse {
+  int* cnt;
+  int* xcc;
+  void* state;
+  float* out;
+  int nsplit, n_heads, n_kv;
+};
+int attn_fuse_ints(int n_kv);
+
 // Decode attention at position state->pos: q = the rotated, pre-scaled queries
 // [Hq*hd] (the QKV GEMV's GEMV_QKV output), keys and values = cache positions
 // [0, pos] (the new position already appended by that GEMV); splits of 64
 // positions (grid nsplit x Hkv, nsplit = attn_decode_splits(max_seq)) merged
 // into out [Hq*hd] fp32.
+// fuse != nullptr merges in the last split block where the launch allows it.
 hipError_t launch_attn_decode(bool kv_bf16, const float* q, int Hq, KvLayout kv,
                               const void* state, int nsplit, float* part_o, float* part_ml,
-                              float* out, hipStream_t st);
+                              float* out, const AttnFuse* fuse, hipStream_t st);
 int attn_decode_splits(int max_seq);
 bool attn_group_supported(int G);
 

@@ -81,7 +81,7 @@ __global__ void k_reset_state(DecodeState* st) {
   st->pos = 0;
   st->token = 0;
   st->bad = 0;
-  st->pad = 0;
+  st->fault = 0;
 }
 
 hipError_t launch_reset_state(void* state, hipStream_t st) {
@@ -101,6 +101,17 @@ hipError_t launch_set_token(void* state, int token, hipStream_t st) {
 __global__ void k_init_block_table(int32_t* table, int n_pages) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n_pages) table[i] = n_pages - 1 - i;
+}
+
+__global__ void k_fill_i32(int32_t* p, int n, int v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+hipError_t launch_fill_i32(int32_t* p, int n, int v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_i32, dim3((n + 255) / 256), dim3(256), 0, st, p, n, v);
+  return hipGetLastError();
 }
 
 hipError_t launch_init_block_table(int32_t* table, int n_pages, hipStream_t st) {
@@ -229,6 +240,58 @@ hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
   return hipGetLastError();
 }
 
+// ---- plain streaming read (the bandwidth ceiling the decode GEMVs are held to) ----------
+// Workgroup b of G reads the 16 KiB blocks b, b + G, b + 2G, ... of the buffer:
+// four non-temporal 16-byte loads per lane per block, all issued before any is
+// used.  The XOR of every loaded word keeps the loads from being dropped; one
+// word per thread is written (never read).
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+__global__ __launch_bounds__(256) void k_stream_read(const u32x4* __restrict__ p, size_t blocks,
+                                                     unsigned* __restrict__ sink) {
+  unsigned acc = 0;
+  for (size_t b = blockIdx.x; b < blocks; b += gridDim.x) {
+    const u32x4* q = p + b * 1024 + threadIdx.x;
+    const u32x4 v0 = __builtin_nontemporal_load(q);
+    const u32x4 v1 = __builtin_nontemporal_load(q + 256);
+    const u32x4 v2 = __builtin_nontemporal_load(q + 512);
+    const u32x4 v3 = __builtin_nontemporal_load(q + 768);
+    const u32x4 x = v0 ^ v1 ^ v2 ^ v3;
+    acc ^= x.x ^ x.y ^ x.z ^ x.w;
+  }
+  sink[(size_t)blockIdx.x * 256 + threadIdx.x] = acc;
+}
+
+hipError_t launch_stream_read(const void* buf, size_t bytes, int grid, unsigned* sink,
+                              hipStream_t st) {
+  if (!buf || !sink || grid < 1 || bytes < 16384 || bytes % 16384) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_stream_read, dim3(grid), dim3(256), 0, st,
+                     static_cast<const u32x4*>(buf), bytes / 16384, sink);
+  return hipGetLastError();
+}
+
+// out[0] = XOR of in[0 .. n): one workgroup.  Every 32-bit word of a streamed
+// buffer is XORed into exactly one thread's sink word, so the XOR of a read's
+// sink is the XOR of the whole buffer, whatever the grid.
+__global__ __launch_bounds__(256) void k_xor_reduce(const unsigned* __restrict__ in, int n,
+                                                    unsigned* __restrict__ out) {
+  __shared__ unsigned red[256];
+  unsigned a = 0;
+  for (int i = threadIdx.x; i < n; i += 256) a ^= in[i];
+  red[threadIdx.x] = a;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] ^= red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0];
+}
+
+hipError_t launch_xor_reduce(const unsigned* in, int n, unsigned* out, hipStream_t st) {
+  if (!in || !out || n < 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_xor_reduce, dim3(1), dim3(256), 0, st, in, n, out);
+  return hipGetLastError();
+}
+
 // ---- argmax, second pass -------------------------------------------------------------
 __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restrict__ part,
                                                         int n, DecodeState* st,
@@ -271,6 +334,7 @@ __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restr
       mirror->bad = bad;
       mirror->token = tok;
       mirror->pos = pos;
+      mirror->fault = st->fault;
     }
   }
 }

@@ -42,7 +42,7 @@ struct Layout {
   size_t kv_layer_stride, kv_bytes;
   // scratch
   size_t x, a, qkv, att, h, kpart, logits, parts, part_o, part_ml, tokens, table, state, hist,
-      seqs;
+      seqs, attn_sync;
   size_t scratch_bytes;
   int nsplit;
 };
@@ -138,6 +138,8 @@ Layout make_layout(const wici_config& c) {
   L.state = o; o = align_up(o + sizeof(DecodeState));
   L.hist = o; o = align_up(o + (size_t)c.max_seq * 4);  // token emitted after each position
   L.seqs = o; o = align_up(o + (size_t)kMaxBatch * sizeof(wici::SeqDesc));  // batched decode
+  // counters and XCD records of the decode attention's in-launch merge
+  L.attn_sync = o; o = align_up(o + (size_t)wici::attn_fuse_ints(c.n_kv_heads) * 4);
   L.scratch_bytes = o;
   return L;
 }
@@ -286,7 +288,18 @@ hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers 
     disarm();                   \
     if (e) return e;            \
   } while (0)
-  WICI_STEP(wici::launch_embed(wb, m->dw + L.embed, c.vocab, d, nullptr, 1, st, x, s));
+  wici::AttnFuse fuse{};
+  fuse.cnt = m->S<int>(L.attn_sync);
+  fuse.xcc = fuse.cnt + wici::attn_fuse_ints(c.n_kv_heads) / 2;
+  fuse.state = st;
+  // bf16 weights: the first QKV projection gathers the embedding row itself (its
+  // profiling slot stays, at zero time)
+  const bool fold_embed = wb == WICI_BF16;
+  if (fold_embed) {
+    if (timers) timers->push_back(wici::LaunchTimer{nullptr, nullptr});
+  } else {
+    WICI_STEP(wici::launch_embed(wb, m->dw + L.embed, c.vocab, d, nullptr, 1, st, x, s));
+  }
   for (int l = 0; l < c.n_layers; ++l) {
     wici::QkvRope rope{};
     rope.cos_t = m->W<float>(L.rope_cos);
@@ -296,11 +309,13 @@ hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers 
     rope.kv_bf16 = kb ? 1 : 0;
     rope.n_q = c.n_heads;
     rope.q_scale = 1.0f / std::sqrt((float)c.head_dim);
+    rope.embed = fold_embed && l == 0 ? m->dw + L.embed : nullptr;
     WICI_STEP(wici::launch_gemv(wb, wici::GEMV_QKV, m->dw + m->layer(l, L.l_wqkv), nqkv, d, x,
                                 m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, qkv, nullptr,
                                 nullptr, s, &rope));
     WICI_STEP(wici::launch_attn_decode(kb, qkv, c.n_heads, m->kv(l), st, L.nsplit,
-                                       m->S<float>(L.part_o), m->S<float>(L.part_ml), att, s));
+                                       m->S<float>(L.part_o), m->S<float>(L.part_ml), att,
+                                       kb ? &fuse : nullptr, s));
     WICI_STEP(wici::launch_gemv(wb, wici::GEMV_RESID, m->dw + m->layer(l, L.l_wo), d, qd, att,
                                 nullptr, 0.f, x, nullptr, nullptr, s));
     WICI_STEP(wici::launch_gemv(wb, wici::GEMV_SWIGLU, m->dw + m->layer(l, L.l_wgu), 2 * F, d, x,
@@ -482,6 +497,16 @@ hipError_t alloc_state_mirror(wici_model* m) {
   return hipHostGetDevicePointer((void**)&m->d_state_mirror, m->h_state, 0);
 }
 
+// The decode attention's in-launch merge found the split blocks of a KV head
+// on different XCDs, so partials may have been read before they were visible:
+// the results of the step cannot be trusted and the model stops here.
+wici_status placement_fault(wici_model* m) {
+  m->failed = true;
+  m->have_token = false;
+  return fail(m, WICI_E_HIP, "decode attention: the split blocks of a KV head did not all run "
+                             "on one XCD (workgroups not dealt to the XCDs in turn)");
+}
+
 // The step's final argmax kernel has written the new state into the pinned
 // mirror m->h_state as well; it is read once the stream has drained.
 wici_status finish_step(wici_model* m, int32_t* tok, float* logits) {
@@ -490,6 +515,7 @@ wici_status finish_step(wici_model* m, int32_t* tok, float* logits) {
                               hipMemcpyDeviceToHost, m->stream));
   HIP_TRY(m, hipStreamSynchronize(m->stream));
   m->pos = m->h_state->pos;
+  if (m->h_state->fault) return placement_fault(m);
   if (m->h_state->bad) {
     m->have_token = false;
     return fail(m, WICI_E_NUMERIC, "non-finite logits at position %d", m->pos - 1);
@@ -587,6 +613,8 @@ wici_status wici_bind_memory(wici_model* m, void* d_weights, size_t weight_bytes
   HIP_TRY(m, hipMemcpy(m->dw + m->L.rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice));
   HIP_TRY(m, wici::launch_init_block_table(m->S<int32_t>(m->L.table), m->L.n_pages, m->stream));
   HIP_TRY(m, wici::launch_reset_state(m->ds + m->L.state, m->stream));
+  HIP_TRY(m, wici::launch_fill_i32(m->S<int32_t>(m->L.attn_sync),
+                                   wici::attn_fuse_ints(m->cfg.n_kv_heads), 0, m->stream));
   HIP_TRY(m, hipStreamSynchronize(m->stream));
   m->bound = true;
   m->pos = 0;
@@ -794,6 +822,10 @@ wici_status wici_decode_n(wici_model* m, int32_t token_in, int32_t n, int32_t* t
   HIP_TRY(m, hipStreamSynchronize(m->stream));
   m->pos = m->h_state->pos;
   const int32_t steps = m->pos - pos0;
+  if (m->h_state->fault) {
+    *n_done = 0;
+    return placement_fault(m);
+  }
   if (m->h_state->bad) {
     m->have_token = false;
     *n_done = steps - 1;
@@ -831,8 +863,8 @@ wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* n
   hipError_t e3 = hipSuccess;
   if (e2 == hipSuccess)
     for (const wici::LaunchTimer& t : tv) {
-      float ms = 0.f;
-      const hipError_t r = hipEventElapsedTime(&ms, t.start, t.stop);
+      float ms = 0.f;  // a slot without events: a step folded into another launch
+      const hipError_t r = t.start ? hipEventElapsedTime(&ms, t.start, t.stop) : hipSuccess;
       if (r != hipSuccess && e3 == hipSuccess) e3 = r;
       durations_ms[n++] = ms;
     }
@@ -866,6 +898,8 @@ wici_status wici_bind_memory_shared(wici_model* m, const wici_model* src, void* 
   HIP_TRY(m, alloc_state_mirror(m));
   HIP_TRY(m, wici::launch_init_block_table(m->S<int32_t>(m->L.table), m->L.n_pages, m->stream));
   HIP_TRY(m, wici::launch_reset_state(m->ds + m->L.state, m->stream));
+  HIP_TRY(m, wici::launch_fill_i32(m->S<int32_t>(m->L.attn_sync),
+                                   wici::attn_fuse_ints(m->cfg.n_kv_heads), 0, m->stream));
   HIP_TRY(m, hipStreamSynchronize(m->stream));
   m->loaded.assign(m->specs.size(), 1);
   m->n_loaded = (int)m->specs.size();
@@ -913,6 +947,9 @@ wici_status wici_decode_batch(wici_model* const* models, int32_t n, const int32_
     sd[b].state = mb->ds + mb->L.state;
     sd[b].hist = mb->S<int32_t>(mb->L.hist);
   }
+  // one sequence: its own step graph (the weight-streaming GEMVs), which the
+  // batched matrix products cannot beat at a single row
+  if (n == 1) return wici_decode_step(lead, tokens_in ? tokens_in[0] : -1, next_tokens, logits);
   for (int b = 0; b < n; ++b)
     if (tokens_in && tokens_in[b] >= 0)
       HIP_TRY(lead, wici::launch_set_token(models[b]->ds + models[b]->L.state, tokens_in[b],
@@ -968,6 +1005,36 @@ wici_status wici_reset_kv(wici_model* m) {
   HIP_TRY(m, hipStreamSynchronize(m->stream));
   m->pos = 0;
   m->have_token = false;
+  return WICI_OK;
+}
+
+wici_status wici_stream_read(const void* d_buf, size_t bytes, int32_t grid, int32_t reps,
+                             void* d_sink, void* hip_stream, float* ms_per_read,
+                             uint32_t* checksum) {
+  if (!d_buf || !d_sink || !ms_per_read || grid < 1 || grid > 65536 || reps < 1 ||
+      bytes < 16384 || bytes % 16384)
+    return WICI_E_ARG;
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  unsigned* sink = static_cast<unsigned*>(d_sink);
+  hipEvent_t a = nullptr, b = nullptr;
+  hipError_t e = hipEventCreate(&a);
+  if (e == hipSuccess) e = hipEventCreate(&b);
+  if (e == hipSuccess) e = hipEventRecord(a, s);
+  for (int i = 0; i < reps && e == hipSuccess; ++i)
+    e = wici::launch_stream_read(d_buf, bytes, grid, sink, s);
+  if (e == hipSuccess) e = hipEventRecord(b, s);
+  if (e == hipSuccess && checksum) {
+    const size_t n = (size_t)256 * grid;
+    e = wici::launch_xor_reduce(sink, (int)n, sink + n, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(checksum, sink + n, 4, hipMemcpyDeviceToHost, s);
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  if (e != hipSuccess) return WICI_E_HIP;
+  *ms_per_read = ms / reps;
   return WICI_OK;
 }
 
