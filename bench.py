@@ -91,6 +91,37 @@ def profile_pass(model, cfg, prompt, n_decode):
     return mean, per_token
 
 
+def stream_ceiling(nbytes=4 << 30, grids=(512, 768, 1024), reps=5):
+    """The plain streaming-read rate of this GPU's memory, measured in this run
+    with the library's own read kernel (wici_stream_read): the best of a few
+    launch shapes, each after one untimed read.  Returns (bytes/s, details)."""
+    import torch
+
+    from paper_2608_24204_amd import binding
+    buf = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(max(grids) * 1024 + 4, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    per = {}
+    for g in grids:
+        binding.stream_read(buf, g, 1, sink)
+        per[g] = binding.stream_read(buf, g, reps, sink)
+    del buf, sink
+    best = min(per, key=per.get)
+    return nbytes / (per[best] / 1e3), {"bytes": nbytes, "reps": reps, "best_grid": best,
+                                        "ms_per_read": {str(g): v for g, v in per.items()}}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg, w, n_prompt, n_decode):
     """The float64 oracle on the host cores over a bounded sample of the workload
     (a shorter prompt, a few decode steps); returns the sample's ids and logits so
@@ -122,7 +153,7 @@ def cpu_baseline(cfg, w, n_prompt, n_decode):
                      f"{'quantised by the oracle and ' if cfg.weight_dtype == 'q8' else ''}"
                      f"widened to float64 beforehand, {conv_s:.1f} s, not timed)",
            "prefill_tok_s": n_prompt / (t1 - t0), "ttft_ms": (t1 - t0) * 1e3,
-           "host_cpus": os.cpu_count()}
+           "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}
     return out, (prompt, ids, logs)
 
 
@@ -235,7 +266,8 @@ def main(argv=None):
     ap.add_argument("--prefill-mode", default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
-    ap.add_argument("--cpu-prompt", type=int, default=128)
+    ap.add_argument("--cpu-prompt", type=int, default=None,
+                    help="prompt ids of the oracle sample (default: the workload's prompt)")
     ap.add_argument("--cpu-decode", type=int, default=3)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before the timed region, copy MIB MiB device-to-device (a plain "
@@ -284,6 +316,9 @@ def main(argv=None):
         torch.cuda.synchronize()
         log(f"calibration copy of {args.calibrate_copy} MiB done")
         del src, dst
+    log("stream-read ceiling")
+    ceil_bps, ceil_info = stream_ceiling()
+    log(f"stream-read ceiling {ceil_bps / 1e9:.0f} GB/s")
     for i in range(args.warmup):
         ttft, dec, _ = run_request(model, prompt, n_decode)
         log(f"warmup {i}: ttft {ttft * 1e3:.2f} ms, decode {n_decode / dec:.1f} tok/s")
@@ -323,6 +358,9 @@ def main(argv=None):
         "ttft_ms": ttft_ms, "prefill_tok_s": cfg.prompt_len / (ttft_ms / 1e3),
         "decode_bytes_per_token": bytes_tok,
         "decode_hbm_frac": bytes_tok * decode_tok_s / HBM_PEAK,
+        "stream_read_ceiling_gbs": ceil_bps / 1e9,
+        "decode_frac_of_stream_ceiling": bytes_tok * decode_tok_s / ceil_bps,
+        "stream_read": ceil_info,
         "prefill_flops": pf_flops,
         "prefill_mfma_frac": pf_flops / (ttft_ms / 1e3) / MFMA_BF16_PEAK,
         "prefill_mode": args.prefill_mode or ("f32" if cfg.weight_dtype == "f32" else "bf16x3"),
@@ -348,7 +386,8 @@ def main(argv=None):
 
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle sample)")
-        cb, (sp, sids, slogs) = cpu_baseline(cfg, w, args.cpu_prompt, args.cpu_decode)
+        cb, (sp, sids, slogs) = cpu_baseline(cfg, w, args.cpu_prompt or cfg.prompt_len,
+                                             args.cpu_decode)
         # same sample through the GPU path
         model.reset_kv()
         g_ids, g_logs = model.generate(sp, args.cpu_decode, want_logits=True)
