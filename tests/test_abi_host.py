@@ -216,3 +216,34 @@ def test_cached_load_checks_arguments():
         assert lib.wici_load_weights_cached(h, t, None, 1, b"/tmp", -1, out) == binding.WICI_E_ARG
     finally:
         lib.wici_destroy(h)
+
+
+def test_cached_load_rejects_data_that_does_not_match_its_hash(tmp_path):
+    """A store miss with both a hash and data saves the data under that hash,
+    so the library hashes the data first: a wrong hash is an argument error
+    (before anything is uploaded), the right one passes that check."""
+    lib = binding.load_library()
+    c = _cfg()
+    h = ctypes.c_void_p()
+    assert lib.wici_create(ctypes.byref(c), None, ctypes.byref(h)) == binding.WICI_OK
+    try:
+        data = np.arange(c.d_model, dtype=np.float32)
+        t = (binding.WiciTensor * 1)()
+        t[0].name = b"norm"
+        t[0].dtype = binding.WICI_F32
+        t[0].ndim = 1
+        t[0].shape[0] = c.d_model
+        t[0].data = data.ctypes.data
+        out = (ctypes.c_int32 * 1)()
+        good = binding.md5(data)
+        bad = bytes([good[0] ^ 1]) + good[1:]
+        store = str(tmp_path).encode()
+        for digest, want in ((bad, binding.WICI_E_ARG), (good, binding.WICI_E_STATE)):
+            hb = (ctypes.c_uint8 * 16).from_buffer_copy(digest)
+            # threshold 0: the tensor goes through the store; the model has no
+            # memory bound yet, so a hash that passes stops at the upload
+            assert lib.wici_load_weights_cached(h, t, hb, 1, store, 0, out) == want
+        assert not os.listdir(tmp_path)
+    finally:
+        lib.wici_destroy(h)
+

@@ -1,6 +1,8 @@
 """Content-addressed weight loading (wici_load_weights_cached) on the GPU: the
 paper's model-caching exchange (hashes first, tensors only on a miss) through the
-C ABI, with the model's outputs bitwise equal to a plain upload's."""
+C ABI.  A model loaded from the store must match the float64 oracle (greedy ids
+identical, logits within 2e-2 of the largest) and be bitwise equal to a plain
+upload."""
 
 from __future__ import annotations
 
@@ -10,6 +12,7 @@ import numpy as np
 import pytest
 
 from paper_2608_24204_amd import configs, inputs
+from tests.parity import compare, oracle_run
 
 pytestmark = pytest.mark.gpu
 
@@ -56,7 +59,7 @@ def test_cache_exchange_matches_plain_upload(cuda_ok, tmp_path):
         m1.close()
     assert ids1 == ids0 and np.array_equal(lg1, lg0)
 
-    # warm store, hashes only for the large tensors: all hits, data never read
+    # warm store, hashes only for the large tensors (sent without data): all hits
     hashes = {n: md5(w[n]) for n in big}
     m2 = WiciModel(CFG)
     try:
@@ -66,6 +69,12 @@ def test_cache_exchange_matches_plain_upload(cuda_ok, tmp_path):
     finally:
         m2.close()
     assert ids2 == ids0 and np.array_equal(lg2, lg0)
+    # the model loaded from the store against the oracle's own greedy run
+    rep = compare(ids2, list(lg2), *oracle_run(CFG, inputs.weights_f64(CFG, w), prompt,
+                                                CFG.decode_steps))
+    print(f"[cache parity] {rep.summary()}", flush=True)
+    assert rep.max_rel_err <= 2e-2
+    assert rep.strict_ids, rep.summary()
 
     # one file missing and one of the wrong size: both needed; resend with data
     lost, bad = sorted(big)[:2]

@@ -156,6 +156,9 @@ def test_kv_cache_holds_oracle_values(cuda_ok):
             g = inputs.bf16_bits_to_f32(bits).astype(np.float64)
             assert np.array_equal(g, oracle.bf16_round(g))   # stored as bf16 values
             scale = np.max(np.abs(o))
+            excess = float(np.max(np.abs(g - o) - np.abs(o) * 2.0 ** -7) / scale)
+            print(f"[kv cache] layer {l}: differ {np.mean(g != o):.4f}, worst excess over one "
+                  f"bf16 step {excess:.3g} of max|o|", flush=True)
             if l == 0:
                 # layer 0 sees exact inputs: both sides round a value they computed
                 # to bf16 and the GPU's value carries only float32 rounding, so the
