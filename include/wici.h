@@ -313,6 +313,22 @@ wici_status wici_stream_read(const void* d_buf, size_t bytes, int32_t grid, int3
                              void* d_sink, void* hip_stream, float* ms_per_read,
                              uint32_t* checksum);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that must not allocate, harnesses that forbid it): one read of
+ * d_buf exactly as wici_stream_read with grid workgroups, but its workspace is
+ * the library's own file-scope device array, so the call allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine).  The array holds the
+ * partial results of at most 4096 workgroups (4 MiB + 256 bytes per GPU, held
+ * until the process ends).  Its device address is looked up once per device on
+ * the first call there.  Every call on a GPU shares that GPU's array, so calls
+ * that overlap on one GPU race.  Each call writes every partial it reads, so
+ * nothing needs clearing.  checksum (host) receives the XOR of every 32-bit word
+ * of the buffer; no time is taken.  Synchronous on hip_stream (NULL: the null
+ * stream).  Errors: WICI_E_ARG (NULL pointers, bytes not a positive multiple of
+ * 16384, grid outside [1, 4096]), WICI_E_HIP (a HIP call failed). */
+wici_status wici_stream_read_noalloc(const void* d_buf, size_t bytes, int32_t grid,
+                                     void* hip_stream, uint32_t* checksum);
+
 /* Message of the last failed call on this model ("" if none).  Valid until the
  * next call on the model. */
 const char* wici_last_error(const wici_model* m);

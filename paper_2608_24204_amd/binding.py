@@ -30,7 +30,7 @@ EXPORTED = ["wici_create", "wici_memory_requirements", "wici_bind_memory", "wici
             "wici_prefill", "wici_decode_step", "wici_decode_n", "wici_reset_kv", "wici_position",
             "wici_read_kv", "wici_profile_decode_step", "wici_quantize_q8", "wici_md5",
             "wici_load_weights_cached", "wici_bind_memory_shared", "wici_decode_batch",
-            "wici_stream_read", "wici_last_error", "wici_destroy"]
+            "wici_stream_read", "wici_stream_read_noalloc", "wici_last_error", "wici_destroy"]
 
 
 class WiciConfig(ctypes.Structure):
@@ -93,6 +93,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
         "wici_decode_batch": ([P, i32, P, P, P], ctypes.c_int),
         "wici_stream_read": ([P, sz, i32, i32, P, P, ctypes.POINTER(ctypes.c_float), P],
                              ctypes.c_int),
+        "wici_stream_read_noalloc": ([P, sz, i32, P, ctypes.POINTER(ctypes.c_uint32)],
+                                     ctypes.c_int),
         "wici_last_error": ([P], ctypes.c_char_p),
         "wici_destroy": ([P], None),
     }

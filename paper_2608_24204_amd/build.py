@@ -21,7 +21,7 @@ BUILD = os.path.join(PKG, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["gemv.hip", "misc.hip", "attention.hip", "gemm.hip", "batch.hip", "model.cpp", "quant.cpp",
-           "cache.cpp"]
+           "cache.cpp", "noalloc.cpp"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
