@@ -363,7 +363,7 @@ def main(argv=None):
         "stream_read": ceil_info,
         "prefill_flops": pf_flops,
         "prefill_mfma_frac": pf_flops / (ttft_ms / 1e3) / MFMA_BF16_PEAK,
-        "prefill_mode": args.prefill_mode or ("f32" if cfg.weight_dtype == "f32" else "bf16x3"),
+        "prefill_mode": args.prefill_mode or ("f32" if cfg.weight_dtype == "f32" else "bf16x3q"),
         "decode_n_tok_s": n_decode * args.steps / sum(dn),
         "decode_n_hbm_frac": bytes_tok * n_decode * args.steps / sum(dn) / HBM_PEAK,
     }

@@ -63,8 +63,15 @@ typedef enum {
                               bf16 terms (two products per tile), ~2^-16 relative */
   WICI_PREFILL_BF16 = 1,   /* matrix cores, bf16; activations rounded to bf16 once */
   WICI_PREFILL_F32 = 2,    /* vector fp32 (required for fp32 weights) */
-  WICI_PREFILL_BF16X3 = 3  /* matrix cores, bf16; three bf16 terms per activation
+  WICI_PREFILL_BF16X3 = 3, /* matrix cores, bf16; three bf16 terms per activation
                               (three products per tile), fp32-accurate */
+  WICI_PREFILL_BF16X3Q = 4 /* matrix cores, bf16; three bf16 terms stored, the Q/K/V
+                              projection reads all three and the O, gate/up and down
+                              projections the first two (the cached keys and values
+                              carry the prompt's precision into every decode step;
+                              the other products' ~2^-16 leaves the workloads'
+                              greedy ids unchanged, measured), 18-26% less prefill
+                              time than BF16X3 */
 } wici_prefill_mode;
 
 enum { WICI_FLAG_NO_GRAPH = 1 }; /* run decode steps eagerly instead of replaying a graph */
@@ -87,6 +94,13 @@ typedef struct {
   int32_t kv_page;        /* positions per KV page: 16, 32, 64 or 128 */
   int32_t prefill_mode;   /* wici_prefill_mode; F32 is required when weight_dtype is F32 */
   int32_t flags;          /* WICI_FLAG_* */
+  int32_t prefill_planes; /* 0: every prefill product reads the activation terms
+                             prefill_mode says.  Else (WICI_PREFILL_BF16X3 only)
+                             the number of the three bf16 terms each product reads,
+                             two bits each (1..3): bits 0-1 the Q/K/V projection,
+                             2-3 the O projection, 4-5 gate/up, 6-7 down; a product
+                             reading fewer terms does less matrix work and carries
+                             its activations to ~2^-16 (two) or ~2^-8 (one) */
 } wici_config;
 
 /* One named weight tensor in logical [out, in] row-major layout.  Names:

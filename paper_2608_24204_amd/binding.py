@@ -22,7 +22,7 @@ WICI_OK, WICI_E_ARG, WICI_E_STATE, WICI_E_CAPACITY, WICI_E_HIP, WICI_E_NUMERIC =
 STATUS_NAMES = {0: "WICI_OK", -1: "WICI_E_ARG", -2: "WICI_E_STATE", -3: "WICI_E_CAPACITY",
                 -4: "WICI_E_HIP", -5: "WICI_E_NUMERIC"}
 WICI_F32, WICI_BF16, WICI_Q8 = 0, 1, 2
-PREFILL_MODES = {"bf16x2": 0, "bf16": 1, "f32": 2, "bf16x3": 3}
+PREFILL_MODES = {"bf16x2": 0, "bf16": 1, "f32": 2, "bf16x3": 3, "bf16x3q": 4}
 WICI_FLAG_NO_GRAPH = 1
 
 # every entry point include/wici.h declares
@@ -42,6 +42,7 @@ class WiciConfig(ctypes.Structure):
         ("kv_dtype", ctypes.c_int32), ("max_seq", ctypes.c_int32),
         ("prefill_chunk", ctypes.c_int32), ("kv_page", ctypes.c_int32),
         ("prefill_mode", ctypes.c_int32), ("flags", ctypes.c_int32),
+        ("prefill_planes", ctypes.c_int32),
     ]
 
 
@@ -109,9 +110,11 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
 
 def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool = True,
                 max_seq: int | None = None, prefill_chunk: int | None = None,
-                kv_page: int | None = None) -> WiciConfig:
+                kv_page: int | None = None, prefill_planes=None) -> WiciConfig:
+    """prefill_planes: None/0 for prefill_mode's own term count, or a tuple
+    (qkv, o, gate_up, down) of bf16 terms each projection reads (bf16x3 only)."""
     if prefill_mode is None:
-        prefill_mode = "f32" if cfg.weight_dtype == "f32" else "bf16x3"
+        prefill_mode = "f32" if cfg.weight_dtype == "f32" else "bf16x3q"
     c = WiciConfig()
     c.n_layers, c.d_model, c.n_heads = cfg.n_layers, cfg.d_model, cfg.n_heads
     c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab = cfg.n_kv_heads, cfg.head_dim, cfg.ffn_dim, cfg.vocab
@@ -124,6 +127,9 @@ def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool =
     c.kv_page = cfg.kv_page if kv_page is None else kv_page
     c.prefill_mode = PREFILL_MODES[prefill_mode]
     c.flags = 0 if graph else WICI_FLAG_NO_GRAPH
+    if prefill_planes:
+        q, o, gu, dn = prefill_planes
+        c.prefill_planes = q | (o << 2) | (gu << 4) | (dn << 6)
     return c
 
 
@@ -234,16 +240,18 @@ class WiciModel:
     def __init__(self, cfg: ModelConfig, *, prefill_mode: str | None = None, graph: bool = True,
                  max_seq: int | None = None, prefill_chunk: int | None = None,
                  kv_page: int | None = None, device: int = 0,
-                 share_weights_of: "WiciModel | None" = None):
+                 share_weights_of: "WiciModel | None" = None, prefill_planes=None):
         """share_weights_of: another (loaded) model whose weights this one uses
-        (wici_bind_memory_shared); only the KV cache and scratch are allocated."""
+        (wici_bind_memory_shared); only the KV cache and scratch are allocated.
+        prefill_planes: see make_config."""
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("WiciModel needs a HIP GPU")
         self.cfg = cfg
         self.lib = load_library()
         self.device = torch.device("cuda", device)
-        self.c = make_config(cfg, prefill_mode, graph, max_seq, prefill_chunk, kv_page)
+        self.c = make_config(cfg, prefill_mode, graph, max_seq, prefill_chunk, kv_page,
+                             prefill_planes)
         wb, kb, sb = memory_requirements(self.c)
         self.mem_bytes = (wb, kb, sb)
         self.stream = torch.cuda.Stream(self.device)

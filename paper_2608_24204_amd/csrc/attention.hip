@@ -5,11 +5,14 @@
 // head's group with it (GQA), so every cached byte is read once per step.  The
 // new position's k/v are rotated, rounded to the storage type, written to the
 // cache and used straight from LDS (no block reads a position another block of
-// the same launch writes).  A second small kernel merges the splits.
+// the same launch writes).  The splits are merged by a second small kernel, or,
+// for a bf16 cache with few splits, by the last split block of each head in the
+// same launch (through the L2 of the XCD all of that head's blocks run on).
 //
 // Prefill: one block per (64 queries, query head), keys streamed through LDS in
 // blocks of 64 with an online softmax; on the matrix cores for a bf16 cache (the
 // fp32 query and probabilities split into bf16 terms), else fp32 vector code.
+#include "attn_decode.h"
 #include "common.h"
 #include "kernels.h"
 #include "launch.h"
@@ -32,13 +35,11 @@ __device__ __forceinline__ size_t kv_off(const KvLayout& kv, int pos, int which,
 // projection's epilogue), so a block's loads depend only on its page-table
 // entries and on the position, which arrive together: every slot of the chunk
 // is then requested at once (slots past the context are loaded and ignored).
-// Each block writes
-// its unnormalised output and (max, sum) statistics; a second kernel merges the
-// splits.  (Merging in the last block of each head would need device-scope
-// fences, whose L2 write-back and invalidate on every block cost more than the
-// extra launch.)
-constexpr int kChunk = 64;       // positions per decode split (at most one per lane of a wave:
-                                 // the softmax statistics take one position per lane)
+// Each block writes its unnormalised output and (max, sum) statistics; a second
+// kernel merges the splits.  (Merging in the last block of each head through
+// device-scope fences, whose L2 write-back and invalidate fall on every block,
+// measured slower than the extra launch; the matrix-core kernel merges in the
+// last block only through one XCD's L2, see attn_merge_in_last_split.)
 constexpr int kMaxSplits = 256;  // splits the merge kernel holds in LDS
 
 // With seqs != nullptr the launch is batched: blockIdx.z is the sequence, whose
@@ -226,131 +227,6 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
 // the registers are held to 96 per lane, so five workgroups share a CU (the LDS
 // allows five): a long context's grid (8 KV heads x 129 splits at 8.2K
 // positions) then fits the chip in one round instead of leaving a tail.
-typedef short short4_t __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
-
-// Merge of a KV head's splits in the last of its split blocks to finish (the
-// batch-1 launch of k_attn_decode_mfma with FUSE, at most kFuseMaxSplits splits).
-// Every split of head g runs on the same XCD, so the blocks exchange their
-// partials through that XCD's L2 alone: each block's stores are acknowledged by
-// the L2 (a wait for all of them) before it takes a ticket from the head's
-// counter, an atomic performed in the same L2.  The block drawing the last
-// ticket reads the partials with loads that bypass its CU's L1 (another
-// workgroup on the CU may hold an older copy of a line) and merges them:
-// out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s.  It then resets
-// the counter for the next launch.  The placement is checked, not assumed: each
-// block records the XCD it ran on (the hardware's XCC id) and the merging block
-// compares them with its own; a mismatch sets fz.state->fault, which the step
-// reports as an error.
-constexpr int kFuseMaxSplits = 32;
-constexpr int kFuseLine = 64;   // ints per head of the counter and XCD arrays (256 bytes)
-
-__device__ __forceinline__ int xcc_id() {
-  return (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 0xf);
-}
-
-// 16 bytes at byte offset `off` of the buffer `r`, read past the L1 (sc0).
-__device__ __forceinline__ u32x4_t load_l2(__amdgpu_buffer_rsrc_t r, int off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 1);
-}
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, size_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
-}
-
-template <int HD, int G>
-__device__ __forceinline__ void attn_merge_in_last_split(const AttnFuse& fz, int g, int split,
-                                                         int nsplit, int n,
-                                                         const float* part_o,
-                                                         const float* part_ml) {
-  constexpr int COLS = G * HD / 4;      // float4 columns of the group's output
-  constexpr int P = 256 / COLS;         // threads per column (>= 2)
-  constexpr int PER = kFuseMaxSplits / P;
-  __shared__ int s_last;
-  __shared__ float s_w[G][kFuseMaxSplits];
-  __shared__ float4 s_red[P][COLS];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int active = (n + kChunk - 1) / kChunk;
-  const int me = xcc_id();
-  if (tid == 0) fz.xcc[g * kFuseLine + split] = me;
-  // this thread's stores have reached the L2 (the empty asm keeps the compiler
-  // from moving memory operations across the wait)
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0);
-  asm volatile("" ::: "memory");
-  __syncthreads();
-  if (tid == 0) {
-    const int old = __hip_atomic_fetch_add(fz.cnt + g * kFuseLine, 1, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_WORKGROUP);
-    s_last = old == active - 1;
-    if (old == active - 1)
-      __hip_atomic_store(fz.cnt + g * kFuseLine, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  }
-  __syncthreads();
-  if (!s_last) return;
-
-  // the group's partials: column c of splits p, p + P, ... (clamped, all issued at once)
-  const int c = tid % COLS, p = tid / COLS;
-  const int hl = c / (HD / 4), d4 = c % (HD / 4);
-  const int hh = g * G + hl;
-  const __amdgpu_buffer_rsrc_t ro = rsrc(part_o, (size_t)fz.n_heads * nsplit * HD * 4);
-  const __amdgpu_buffer_rsrc_t rm = rsrc(part_ml, (size_t)fz.n_heads * nsplit * 2 * 4);
-  const __amdgpu_buffer_rsrc_t rx = rsrc(fz.xcc, (size_t)fz.n_kv * kFuseLine * 4);
-  u32x4_t pv[PER];
-  if (p < P) {
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int sp = min(p + P * k, active - 1);
-      pv[k] = load_l2(ro, (int)((((size_t)hh * nsplit + sp) * HD + 4 * d4) * 4));
-    }
-  }
-  // statistics: one wavefront per head, lane = split
-  for (int h = wave; h < G; h += 4) {
-    const int hq = g * G + h, sp = min(lane, active - 1);
-    const size_t f = ((size_t)hq * nsplit + sp) * 2;   // float index of (m, l)
-    const u32x4_t st2 = load_l2(rm, (int)((f & ~(size_t)3) * 4));
-    const u32x4_t xv = load_l2(rx, (g * kFuseLine + (sp & ~3)) * 4);
-    // both loads in one round trip (the compiler would otherwise issue the XCD
-    // record's load only inside the branch that tests it, after the reductions)
-    asm volatile("" ::"v"(st2.x), "v"(xv.x));
-    const bool odd = (f & 3) != 0;
-    const float mv = __uint_as_float(odd ? st2.z : st2.x), lv = __uint_as_float(odd ? st2.w : st2.y);
-    const int xo = (int)(xv[sp & 3]);
-    const bool on = lane < active;
-    const float M = wave_max(on ? mv : -INFINITY);
-    const float e = on ? __expf(mv - M) : 0.f;
-    const float L = wave_sum(e * (on ? lv : 0.f));
-    if (on) s_w[h][lane] = e / L;
-    if (on && xo != me) static_cast<DecodeState*>(fz.state)->fault = 1;
-  }
-  __syncthreads();
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (p < P) {
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int sp = p + P * k;
-      if (sp < active) {
-        const float w = s_w[hl][sp];
-        acc.x += w * __uint_as_float(pv[k].x);
-        acc.y += w * __uint_as_float(pv[k].y);
-        acc.z += w * __uint_as_float(pv[k].z);
-        acc.w += w * __uint_as_float(pv[k].w);
-      }
-    }
-    s_red[p][c] = acc;
-  }
-  __syncthreads();
-  if (tid < COLS) {
-    float4 o = s_red[0][tid];
-#pragma unroll
-    for (int q = 1; q < P; ++q) {
-      const float4 t = s_red[q][tid];
-      o.x += t.x; o.y += t.y; o.z += t.z; o.w += t.w;
-    }
-    reinterpret_cast<float4*>(fz.out)[(size_t)g * COLS + tid] = o;
-  }
-}
-
 template <int HD, int G, bool FUSE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G <= 5 && !FUSE ? 5 : 1))) void
 k_attn_decode_mfma(const float* __restrict__ q_in,
@@ -374,13 +250,6 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
     part_o += (size_t)blockIdx.z * heads * HD;
     part_ml += (size_t)blockIdx.z * heads * 2;
   }
-  constexpr int DS = HD / 32;  // 32-deep steps of S^T
-  constexpr int DT = HD / 16;  // 16-wide output tiles of P V
-  constexpr int VP = 16 + 4;   // LDS row of one dimension's 16 positions (8-byte aligned reads)
-  __shared__ bf16_t vt[4][HD][VP];
-  __shared__ float wm[4][G], wl[4][G];
-  __shared__ float wo[4][G][HD];
-
   const int Hkv = kv.n_kv;
   int nsplit, split, g;
   if constexpr (FUSE) {
@@ -396,151 +265,9 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
     split = blockIdx.x;
     g = blockIdx.y;
   }
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int r16 = lane & 15, g4 = lane >> 4;
-  const int start = split * kChunk;
-  const int ps = __ffs(kv.page) - 1;
-  const bf16_t* base = static_cast<const bf16_t*>(kv.base);
-  const size_t head_stride = (size_t)kv.page * HD;
-
-  // this lane's page, its query slice (head r16) and the position.  The compiler
-  // tests the position (the exit below) before it issues the page and query
-  // loads, so those follow in a round trip of their own; a fence that keeps them
-  // ahead of the test (two round trips instead of three) measured slower.
-  const int jl = start + 16 * wave + r16;  // this lane's key/value position
-  const int jc = min(jl, kv.max_pos - 1);
-  const int phys = kv.table[jc >> ps];
-  float qv[DS][8];
-  {
-    const float* qr = q_in + ((size_t)g * G + min(r16, G - 1)) * HD + 8 * g4;
-#pragma unroll
-    for (int s = 0; s < DS; ++s) {
-      const float4 a = *reinterpret_cast<const float4*>(qr + 32 * s);
-      const float4 b = *reinterpret_cast<const float4*>(qr + 32 * s + 4);
-      qv[s][0] = a.x; qv[s][1] = a.y; qv[s][2] = a.z; qv[s][3] = a.w;
-      qv[s][4] = b.x; qv[s][5] = b.y; qv[s][6] = b.z; qv[s][7] = b.w;
-    }
-  }
-  const int n = st->pos + 1;
-  if (start >= n) return;
-
-  // then the keys and values of this lane's position
-  const bf16_t* pk = base + (((size_t)phys * 2 + 0) * Hkv + g) * head_stride +
-                     (size_t)(jc & (kv.page - 1)) * HD + 8 * g4;
-  const bf16_t* pv = pk + (size_t)Hkv * head_stride;
-  bf16x8_t kf[DS];
-  uint4 vr[DS];
-#pragma unroll
-  for (int s = 0; s < DS; ++s) {
-    kf[s] = *reinterpret_cast<const bf16x8_t*>(pk + 32 * s);
-    vr[s] = *reinterpret_cast<const uint4*>(pv + 32 * s);
-  }
-  // the query as three bf16 terms (columns past G are zero)
-  bf16x8_t qb[3][DS];
-#pragma unroll
-  for (int s = 0; s < DS; ++s)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float v = r16 < G ? qv[s][e] : 0.f;
-#pragma unroll
-      for (int t = 0; t < 3; ++t) {
-        const __bf16 b = static_cast<__bf16>(v);
-        qb[t][s][e] = b;
-        v -= static_cast<float>(b);
-      }
-    }
-  // values transposed into this wavefront's LDS tile (zero past the context:
-  // a stale slot may hold anything, and 0 x NaN is NaN)
-  const bool valid = jl < n;
-#pragma unroll
-  for (int s = 0; s < DS; ++s) {
-    const unsigned w4[4] = {vr[s].x, vr[s].y, vr[s].z, vr[s].w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const unsigned w = valid ? w4[e] : 0u;
-      vt[wave][32 * s + 8 * g4 + 2 * e][r16] = (bf16_t)(w & 0xffffu);
-      vt[wave][32 * s + 8 * g4 + 2 * e + 1][r16] = (bf16_t)(w >> 16);
-    }
-  }
-
-  // S^T: lane holds S[position 4 g4 + i][head r16]
-  floatx4_t sc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int s = 0; s < DS; ++s)
-#pragma unroll
-    for (int t = 0; t < 3; ++t)
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qb[t][s], sc, 0, 0, 0);
-  float m = -INFINITY;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (start + 16 * wave + 4 * g4 + i >= n) sc[i] = -INFINITY;
-    m = fmaxf(m, sc[i]);
-  }
-  m = fmaxf(m, __shfl_xor(m, 16));
-  m = fmaxf(m, __shfl_xor(m, 32));
-  float p[4], l = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    p[i] = sc[i] == -INFINITY ? 0.f : __expf(sc[i] - m);
-    l += p[i];
-  }
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
-  // P as three bf16 terms in the A-operand order (head r16, positions 4 g4 + i)
-  short4_t pa[3];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float v = p[i];
-#pragma unroll
-    for (int t = 0; t < 3; ++t) {
-      const __bf16 b = static_cast<__bf16>(v);
-      pa[t][i] = __builtin_bit_cast(short, b);
-      v -= static_cast<float>(b);
-    }
-  }
-  __syncthreads();  // the value tiles are in LDS
-
-  // O = P V: lane holds O[head 4 g4 + i][dimension 16 u + r16]
-  floatx4_t o[DT];
-#pragma unroll
-  for (int u = 0; u < DT; ++u) {
-    o[u] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-    const short4_t vb = *reinterpret_cast<const short4_t*>(&vt[wave][16 * u + r16][4 * g4]);
-#pragma unroll
-    for (int t = 0; t < 3; ++t)
-      o[u] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vb, o[u], 0, 0, 0);
-  }
-  // combine the four wavefronts
-  if (g4 == 0 && r16 < G) { wm[wave][r16] = m; wl[wave][r16] = l; }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int h = 4 * g4 + i;
-    if (h < G) {
-#pragma unroll
-      for (int u = 0; u < DT; ++u) wo[wave][h][16 * u + r16] = o[u][i];
-    }
-  }
-  __syncthreads();
-  for (int idx = tid; idx < G * HD; idx += 256) {
-    const int h = idx / HD, d = idx % HD;
-    float M = wm[0][h];
-#pragma unroll
-    for (int w = 1; w < 4; ++w) M = fmaxf(M, wm[w][h]);
-    float acc = 0.f, L = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float e = wm[w][h] == -INFINITY ? 0.f : __expf(wm[w][h] - M);
-      acc += e * wo[w][h][d];
-      L += e * wl[w][h];
-    }
-    const int hh = g * G + h;
-    part_o[((size_t)hh * nsplit + split) * HD + d] = acc;
-    if (d == 0) {
-      part_ml[((size_t)hh * nsplit + split) * 2 + 0] = M;
-      part_ml[((size_t)hh * nsplit + split) * 2 + 1] = L;
-    }
-  }
-  if constexpr (FUSE) attn_merge_in_last_split<HD, G>(fz, g, split, nsplit, n, part_o, part_ml);
+  const int n = attn_split_mfma<HD, G>(q_in, kv, st, part_o, part_ml, g, split, nsplit);
+  if constexpr (FUSE)
+    if (n > 0) attn_merge_in_last_split<HD, G>(fz, g, split, nsplit, n, part_o, part_ml);
 }
 
 // out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s over the active

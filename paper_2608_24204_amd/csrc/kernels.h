@@ -41,6 +41,22 @@ struct KvLayout {
   //   ((phys * 2 + kv) * n_kv + h) * page * hd + s * hd + d
 };
 
+// The merge of a batch-1 decode attention done by the last split block of each
+// KV head (one launch, no merge kernel), for bf16 caches of up to 32 splits.
+// cnt and xcc each hold 64 ints per KV head (attn_fuse_ints(n_kv) ints in all,
+// cnt first); the counters must be zero before the first launch and are zero
+// again after every launch.  state is the step's DecodeState: its `fault` field
+// is set if the splits of one head did not all run on one XCD (their partials
+// then cannot be trusted).  The launcher fills in the other fields.
+struct AttnFuse {
+  int* cnt;
+  int* xcc;
+  void* state;
+  float* out;
+  int nsplit, n_heads, n_kv;
+};
+int attn_fuse_ints(int n_kv);
+
 // The decode QKV projection's epilogue (GEMV_QKV): RoPE at the current position
 // and the KV-cache append.  W is [(n_q + 2 n_kv) * hd, K] (query heads, then key
 // heads, then value heads); the GEMV walks it in RoPE pairs (rows j and j + hd/2
@@ -148,21 +164,6 @@ hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
                                KvLayout kv, const ActBuf& out, hipStream_t st);
 
-// The merge of a batch-1 decode attention done by the last split block of each
-// KV head (one launch, no merge kernel), for bf16 caches of up to 32 splits.
-// cnt and xcc each hold 64 ints per KV head (attn_fuse_ints(n_kv) ints in all,
-// cnt first); the counters must be zero before the first launch and are zero
-// again after every launch.  state is the step's DecodeState: its `fault` field
-// is set if the splits of one head did not all run on one XCD (their partials
-// then cannot be trusted).  The launcher fills in the other fields.
-struct AttnFuse {
-  int* cnt;
-  int* xcc;
-  void* state;
-  float* out;
-  int nsplit, n_heads, n_kv;
-};
-int attn_fuse_ints(int n_kv);
 
 // Decode attention at position state->pos: q = the rotated, pre-scaled queries
 // [Hq*hd] (the QKV GEMV's GEMV_QKV output), keys and values = cache positions

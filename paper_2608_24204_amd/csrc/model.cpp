@@ -33,6 +33,25 @@ constexpr int kMaxKSplit = 4;   // K ranges of a prefill residual product (parti
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 size_t dsize(int32_t dt) { return dt == WICI_BF16 ? 2 : 4; }
 
+// bf16 activation terms stored for the prefill products, and read by each of them
+struct Planes {
+  int store, qkv, o, gu, down;
+};
+Planes prefill_planes(const wici_config& c) {
+  const int nt = c.prefill_mode == WICI_PREFILL_F32 ? 0
+                 : c.prefill_mode == WICI_PREFILL_BF16 ? 1
+                 : c.prefill_mode == WICI_PREFILL_BF16X2 ? 2 : 3;
+  Planes p{nt, nt, nt, nt, nt};
+  if (c.prefill_mode == WICI_PREFILL_BF16X3Q) p = Planes{3, 3, 2, 2, 2};
+  if (c.prefill_planes) {
+    p.qkv = c.prefill_planes & 3;
+    p.o = (c.prefill_planes >> 2) & 3;
+    p.gu = (c.prefill_planes >> 4) & 3;
+    p.down = (c.prefill_planes >> 6) & 3;
+  }
+  return p;
+}
+
 struct Layout {
   // weights
   size_t l_wqkv, l_wo, l_wgu, l_wdown, l_anorm, l_fnorm, layer_stride;
@@ -73,7 +92,7 @@ bool config_ok(const wici_config* c, std::string* why) {
   if (c->prefill_chunk < 1 || c->prefill_chunk > 8192) return bad("prefill_chunk out of range");
   if (c->kv_page != 16 && c->kv_page != 32 && c->kv_page != 64 && c->kv_page != 128)
     return bad("kv_page must be 16, 32, 64 or 128");
-  if (c->prefill_mode < WICI_PREFILL_BF16X2 || c->prefill_mode > WICI_PREFILL_BF16X3)
+  if (c->prefill_mode < WICI_PREFILL_BF16X2 || c->prefill_mode > WICI_PREFILL_BF16X3Q)
     return bad("bad prefill_mode");
   if (c->weight_dtype == WICI_F32 && c->prefill_mode != WICI_PREFILL_F32)
     return bad("fp32 weights need prefill_mode WICI_PREFILL_F32");
@@ -82,6 +101,13 @@ bool config_ok(const wici_config* c, std::string* why) {
       (c->d_model > 16384 || c->ffn_dim > 16384 || c->n_heads * c->head_dim > 16384))
     return bad("fp32 weights need d_model, ffn_dim and n_heads*head_dim of at most 16384");
   if (c->flags & ~WICI_FLAG_NO_GRAPH) return bad("unknown flags");
+  if (c->prefill_planes != 0) {
+    if (c->prefill_mode != WICI_PREFILL_BF16X3)
+      return bad("prefill_planes needs prefill_mode WICI_PREFILL_BF16X3");
+    if (c->prefill_planes & ~0xff) return bad("prefill_planes has bits above 7");
+    for (int i = 0; i < 4; ++i)
+      if (((c->prefill_planes >> (2 * i)) & 3) == 0) return bad("prefill_planes: a field of 0");
+  }
   if (c->tied_embeddings != 0 && c->tied_embeddings != 1) return bad("tied_embeddings must be 0 or 1");
   return true;
 }
@@ -290,7 +316,7 @@ hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers 
   } while (0)
   wici::AttnFuse fuse{};
   fuse.cnt = m->S<int>(L.attn_sync);
-  fuse.xcc = fuse.cnt + wici::attn_fuse_ints(c.n_kv_heads) / 2;
+  fuse.xcc = fuse.cnt + c.n_kv_heads * 64;
   fuse.state = st;
   // bf16 weights: the first QKV projection gathers the embedding row itself (its
   // profiling slot stays, at zero time)
@@ -346,15 +372,19 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   float* x = m->S<float>(L.x);
   float* qkv = m->S<float>(L.qkv);
   const size_t C = c.prefill_chunk;
-  const int nt = c.prefill_mode == WICI_PREFILL_F32 ? 0
-                 : c.prefill_mode == WICI_PREFILL_BF16 ? 1
-                 : c.prefill_mode == WICI_PREFILL_BF16X2 ? 2 : 3;
+  const Planes pl = prefill_planes(c);
+  const int nt = pl.store;
   auto act = [&](size_t off, size_t width) {
     wici::ActBuf b;
     b.f32 = m->S<float>(off);
     b.planes = m->S<wici::bf16_t>(off);
     b.plane_stride = C * width;
     b.nt = nt;
+    return b;
+  };
+  // the same buffer as a product reads it: its first n terms
+  auto rd = [](wici::ActBuf b, int n) {
+    b.nt = b.nt == 0 ? 0 : n;
     return b;
   };
   const wici::ActBuf a = act(L.a, d), att = act(L.att, qd), h = act(L.h, F);
@@ -369,8 +399,8 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   // (in split order, so the result does not depend on scheduling).
   float* P = m->S<float>(L.kpart);
   const size_t p_split = C * d;
-  const int s_o = wici::gemm_split_count(wb, nt, T, d, qd, kMaxKSplit);
-  const int s_d = wici::gemm_split_count(wb, nt, T, d, F, kMaxKSplit);
+  const int s_o = wici::gemm_split_count(wb, rd(att, pl.o).nt, T, d, qd, kMaxKSplit);
+  const int s_d = wici::gemm_split_count(wb, rd(h, pl.down).nt, T, d, F, kMaxKSplit);
   int pending = 0;  // splits of the previous down product not yet added to x
   auto norm = [&](const float* gain, int nsplit) {
     return nsplit > 1 ? wici::launch_resid_sum_rmsnorm(x, P, nsplit, p_split, gain, c.rms_eps, T,
@@ -385,19 +415,19 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   };
   for (int l = 0; l < c.n_layers; ++l) {
     if ((e = norm(m->W<float>(m->layer(l, L.l_anorm)), pending))) return e;
-    if ((e = wici::launch_gemm(wb, wici::GEMV_STORE, a, d, m->dw + m->layer(l, L.l_wqkv), T,
-                               nqkv, d, qkv, nqkv, none, 0, s)))
+    if ((e = wici::launch_gemm(wb, wici::GEMV_STORE, rd(a, pl.qkv), d,
+                               m->dw + m->layer(l, L.l_wqkv), T, nqkv, d, qkv, nqkv, none, 0, s)))
       return e;
     if ((e = wici::launch_rope_append(kb, qkv, T, p0, c.n_heads, m->W<float>(L.rope_cos),
                                       m->W<float>(L.rope_sin), m->kv(l), s)))
       return e;
     if ((e = wici::launch_attn_prefill(kb, qkv, T, p0, c.n_heads, m->kv(l), att, s))) return e;
-    if ((e = resid(att, qd, m->layer(l, L.l_wo), s_o))) return e;
+    if ((e = resid(rd(att, pl.o), qd, m->layer(l, L.l_wo), s_o))) return e;
     if ((e = norm(m->W<float>(m->layer(l, L.l_fnorm)), s_o))) return e;
-    if ((e = wici::launch_gemm(wb, wici::GEMV_SWIGLU, a, d, m->dw + m->layer(l, L.l_wgu), T,
-                               2 * F, d, nullptr, 0, h, F, s)))
+    if ((e = wici::launch_gemm(wb, wici::GEMV_SWIGLU, rd(a, pl.gu), d,
+                               m->dw + m->layer(l, L.l_wgu), T, 2 * F, d, nullptr, 0, h, F, s)))
       return e;
-    if ((e = resid(h, F, m->layer(l, L.l_wdown), s_d))) return e;
+    if ((e = resid(rd(h, pl.down), F, m->layer(l, L.l_wdown), s_d))) return e;
     pending = s_d;
   }
   if (pending > 1)
@@ -418,15 +448,18 @@ hipError_t enqueue_decode_batch(wici_model* m, int B) {
   const int d = c.d_model, F = c.ffn_dim, qd = c.n_heads * c.head_dim;
   const int nqkv = qd + 2 * c.n_kv_heads * c.head_dim;
   const size_t C = c.prefill_chunk;
-  const int nt = c.prefill_mode == WICI_PREFILL_F32 ? 0
-                 : c.prefill_mode == WICI_PREFILL_BF16 ? 1
-                 : c.prefill_mode == WICI_PREFILL_BF16X2 ? 2 : 3;
+  const Planes pl = prefill_planes(c);
+  const int nt = pl.store;
   auto act = [&](size_t off, size_t width) {
     wici::ActBuf b;
     b.f32 = m->S<float>(off);
     b.planes = m->S<wici::bf16_t>(off);
     b.plane_stride = C * width;
     b.nt = nt;
+    return b;
+  };
+  auto rd = [](wici::ActBuf b, int n) {
+    b.nt = b.nt == 0 ? 0 : n;
     return b;
   };
   const wici::ActBuf a = act(L.a, d), att = act(L.att, qd), h = act(L.h, F);
@@ -452,19 +485,19 @@ hipError_t enqueue_decode_batch(wici_model* m, int B) {
   for (int l = 0; l < c.n_layers; ++l) {
     WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, B, d,
                                        a, s));
-    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_STORE, a, d, m->dw + m->layer(l, L.l_wqkv), B,
+    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_STORE, rd(a, pl.qkv), d, m->dw + m->layer(l, L.l_wqkv), B,
                                nqkv, d, qkv, nqkv, none, 0, s));
     WICI_TRY(wici::launch_rope_append_batch(kb, qkv, B, c.n_heads, m->W<float>(L.rope_cos),
                                             m->W<float>(L.rope_sin), seqs, l, kv, q_scale, s));
     WICI_TRY(wici::launch_attn_decode_batch(kb, qkv, nqkv, B, c.n_heads, kv, seqs, l, L.nsplit,
                                             part_o, part_ml, att, s));
-    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_RESID, att, qd, m->dw + m->layer(l, L.l_wo), B, d,
+    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_RESID, rd(att, pl.o), qd, m->dw + m->layer(l, L.l_wo), B, d,
                                qd, x, d, none, 0, s));
     WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_fnorm)), c.rms_eps, B, d,
                                        a, s));
-    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_SWIGLU, a, d, m->dw + m->layer(l, L.l_wgu), B,
+    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_SWIGLU, rd(a, pl.gu), d, m->dw + m->layer(l, L.l_wgu), B,
                                2 * F, d, nullptr, 0, h, F, s));
-    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_RESID, h, F, m->dw + m->layer(l, L.l_wdown), B, d,
+    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_RESID, rd(h, pl.down), F, m->dw + m->layer(l, L.l_wdown), B, d,
                                F, x, d, none, 0, s));
   }
   WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(L.final_norm), c.rms_eps, B, d, a, s));

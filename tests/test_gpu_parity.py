@@ -125,7 +125,7 @@ def test_long_capacity_decode_attention_head_dim_64(cuda_ok, name, P, max_seq, p
     assert rep.strict_ids, rep.summary()
 
 
-@pytest.mark.parametrize("mode", ["bf16x3", "bf16x2", "bf16", "f32"])
+@pytest.mark.parametrize("mode", ["bf16x3q", "bf16x3", "bf16x2", "bf16", "f32"])
 def test_prefill_modes(cuda_ok, mode):
     cfg = SMALL["gqa64_bf16"]
     prompt = inputs.make_prompt(cfg, 130)
@@ -134,6 +134,29 @@ def test_prefill_modes(cuda_ok, mode):
     if mode != "bf16":
         assert rep.max_rel_err <= 1e-3
         assert rep.strict_ids, rep.summary()
+
+
+def _prefill_logits(cfg, w, prompt, n, **kw):
+    m = make_model(cfg, w, max_seq=len(prompt) + n + 1, **kw)
+    try:
+        ids, logs = m.generate(prompt, n, want_logits=True)
+    finally:
+        m.close()
+    return ids, np.stack(logs)
+
+
+@pytest.mark.parametrize("planes,same_as", [((3, 2, 2, 2), "bf16x3q"), ((3, 3, 3, 3), "bf16x3")])
+def test_prefill_plane_fields_match_whole_modes(cuda_ok, planes, same_as):
+    """Both modes store three bf16 terms (so prefill attention carries its query
+    and probabilities in three terms alike); the per-product fields then choose
+    exactly the terms each product of the whole mode reads, bit for bit."""
+    cfg = SMALL["gqa128_bf16"]
+    w, _ = weights_for(cfg, 0.1)
+    prompt = inputs.make_prompt(cfg, 150)
+    a = _prefill_logits(cfg, w, prompt, 3, prefill_mode="bf16x3", prefill_planes=planes)
+    b = _prefill_logits(cfg, w, prompt, 3, prefill_mode=same_as)
+    assert a[0] == b[0]
+    assert np.array_equal(a[1], b[1])
 
 
 def test_kv_cache_holds_oracle_values(cuda_ok):

@@ -46,7 +46,7 @@ def run(cfg, mode, **kw):
     return rep
 
 
-@pytest.mark.parametrize("mode", ["bf16x3", "f32"])
+@pytest.mark.parametrize("mode", ["bf16x3q", "bf16x3", "f32"])
 @pytest.mark.parametrize("name", list(Q8))
 def test_q8_small_configs_match_oracle(cuda_ok, name, mode):
     rep = run(Q8[name], mode, kv_page=16)
