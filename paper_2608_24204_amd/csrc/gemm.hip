@@ -52,8 +52,9 @@ constexpr int kLDK = 32;  // LDS row (bf16 elements): 64 bytes, four 16-byte chu
 // (4 consecutive rows x 4 chunks, as loaded from global memory) then cover four
 // disjoint 64-byte bank ranges, and sixteen lanes that read a fragment (16 rows,
 // one chunk) cover all 64 banks once: neither access conflicts.
+__device__ __forceinline__ int lds_swz(int row) { return (row >> 2) & 3; }
 __device__ __forceinline__ int lds_chunk(int row, int chunk) {
-  return row * kLDK + 8 * (chunk ^ ((row >> 2) & 3));
+  return row * kLDK + 8 * (chunk ^ lds_swz(row));
 }
 
 // Q8 weights: a step of 32 along K is one quantisation block, so the codes go
@@ -256,10 +257,16 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
 // one is multiplied, with no registers held for them and no register-to-LDS copy.
 // The waits are explicit (this step's loads counted down, then a bare barrier): a
 // __syncthreads would wait for every load in flight.  Rows past M or N fetch the
-// last row (their outputs are dropped).  128 x 128 tile, four wavefronts of 64 x
-// 64.  Two stages (64 KB for three planes) keep two workgroups per CU and beat
-// the register-staged kernel by 12-20% on the 8B projection shapes at 1-2K rows;
-// three stages (96 KB) leave one workgroup per CU and lose 10-20% to it.
+// last row (their outputs are dropped).  Four wavefronts in a 2 x 2 grid, each
+// owning 64 rows x 64 WNT columns: a 128 x 128 WNT block.
+//
+// The loop is bound by LDS traffic, not by the matrix cores: per K step a
+// wavefront reads NT x 4 activation fragments and 4 WNT weight fragments
+// (16 bytes a lane each) for NT x 16 WNT products, and the stage fills write
+// (NT + WNT) x 8 KB per workgroup.  Wider wavefront tiles (WNT = 2) re-read
+// each activation fragment for twice the columns, which cuts the bytes per
+// product by a third or more when the activation has two or three terms.
+// Two stages keep two workgroups per CU (2 x 80 KB at NT = 3, WNT = 2).
 constexpr int kDmaStages = 2;
 
 __device__ __forceinline__ void dma16(const bf16_t* g, bf16_t* lds_wave) {
@@ -272,39 +279,53 @@ __device__ __forceinline__ void wait_vm_lgkm() {
   __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
 }
 
-template <int NT, int EPI, int STG = kDmaStages>
+template <int NT, int EPI, int STG = kDmaStages, int WNT = 1, bool NMAJ = false>
 __global__ __launch_bounds__(256) void k_gemm_dma(const bf16_t* __restrict__ A, size_t a_plane,
                                                   int lda, const bf16_t* __restrict__ W, int M,
                                                   int N, int K, int ks, float* __restrict__ C,
                                                   size_t c_split, int ldc, ActBuf H, int ldh) {
-  constexpr int BM = 128, BN = 128;
+  constexpr int BM = 128, BN = 128 * WNT, FN = 4 * WNT;  // FN: 16-column tiles per wavefront
   constexpr int TILE = 128 * kLDK;            // bf16 elements of one 128-row tile of a step
-  constexpr int STAGE = (NT + 1) * TILE;      // NT activation planes, then the weights
-  constexpr int PER_LANE = (NT + 1) * 2;      // 16-byte units per lane per stage
+  constexpr int STAGE = (NT + WNT) * TILE;    // NT activation planes, then WNT weight tiles
+  constexpr int PER_LANE = (NT + WNT) * 2;    // 16-byte units per lane per stage
   extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
 
-  const int n_mt = (M + BM - 1) / BM, n_nt = (N + BN - 1) / BN, T = n_mt * n_nt;
-  const int per_xcd = (T + 7) / 8;
-  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (t >= T) return;
-  const int m0 = (t / n_nt) * BM, n0 = (t % n_nt) * BN;
+  const int n_mt = (M + BM - 1) / BM, n_nt = (N + BN - 1) / BN;
+  int m0, n0;
+  if (NMAJ) {
+    // each XCD owns a contiguous range of weight column tiles for every row tile,
+    // the row tiles of one column tile on consecutive workgroups (so the blocks
+    // resident on an XCD share weight tiles through its L2)
+    const int nper = (n_nt + 7) / 8, loc = blockIdx.x / 8;
+    const int nt_i = (blockIdx.x % 8) * nper + loc / n_mt;
+    if (nt_i >= n_nt || loc >= nper * n_mt) return;
+    m0 = (loc % n_mt) * BM;
+    n0 = nt_i * BN;
+  } else {
+    const int T = n_mt * n_nt, per_xcd = (T + 7) / 8;
+    const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (t >= T) return;
+    m0 = (t / n_nt) * BM;
+    n0 = (t % n_nt) * BN;
+  }
   const int kbeg = blockIdx.y * ks;
   C += blockIdx.y * c_split;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
 
-  // unit u = (i * 4 + wave) * 64 + lane of a stage holds (matrix u / 512, row
-  // (u % 512) / 4, LDS chunk u % 4), i.e. the row's global chunk (u % 4) ^ sw(row)
+  // unit u = (i * 4 + wave) * 64 + lane of a stage holds (128-row tile u / 512,
+  // row (u % 512) / 4, LDS chunk u % 4), i.e. the row's global chunk
+  // (u % 4) ^ lds_swz(row); tiles 0..NT-1 are the activation planes, NT.. the weights
   const bf16_t* src[PER_LANE];
 #pragma unroll
   for (int i = 0; i < PER_LANE; ++i) {
     const int u = (i * 4 + wave) * 64 + lane, mat = u >> 9, r = (u & 511) >> 2;
-    const int c = (u & 3) ^ ((r >> 2) & 3);
+    const int c = (u & 3) ^ lds_swz(r);
     if (mat < NT)
       src[i] = A + mat * a_plane + (size_t)min(m0 + r, M - 1) * lda + kbeg + c * 8;
     else
-      src[i] = W + (size_t)min(n0 + r, N - 1) * K + kbeg + c * 8;
+      src[i] = W + (size_t)min(n0 + (mat - NT) * 128 + r, N - 1) * K + kbeg + c * 8;
   }
   auto issue = [&](int stage, int kt) {
     bf16_t* sb = smem + stage * STAGE;
@@ -312,29 +333,37 @@ __global__ __launch_bounds__(256) void k_gemm_dma(const bf16_t* __restrict__ A, 
     for (int i = 0; i < PER_LANE; ++i) dma16(src[i] + kt * kBK, sb + (i * 4 + wave) * 512);
   };
 
-  floatx4_t acc[4][4];
+  floatx4_t acc[4][FN];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   const int fr = lane & 15, fk = (lane >> 4) * 8;
 
+  static_assert(STG >= 2 && STG <= 4, "stage ring of 2-4");
   const int KT = ks / kBK;
-  issue(0, 0);
-  if (STG > 2 && KT > 1) issue(1, 1);
+#pragma unroll
+  for (int s = 0; s < STG - 1; ++s)
+    if (s < KT) issue(s, s);
   for (int kt = 0; kt < KT; ++kt) {
-    // this step's units have landed (the next step's may still be in flight) and
-    // every wavefront is done reading the stage the step after next refills
-    if (STG > 2 && kt + 1 < KT) wait_vm_lgkm<PER_LANE>();
+    // this step's units have landed (the next steps' may still be in flight) and
+    // every wavefront is done reading the stage that is refilled next
+    const int ahead = min(STG - 2, KT - 1 - kt);  // later steps already issued
+    if (ahead >= 2) wait_vm_lgkm<2 * PER_LANE>();
+    else if (ahead == 1) wait_vm_lgkm<PER_LANE>();
     else wait_vm_lgkm<0>();
     __builtin_amdgcn_s_barrier();
     if (kt + STG - 1 < KT) issue((kt + STG - 1) % STG, kt + STG - 1);
     const bf16_t* sb = smem + (kt % STG) * STAGE;
-    bf16x8_t bfr[4];
+    // weight fragments: wavefront column block wn covers weight rows
+    // [64 WNT wn, 64 WNT (wn + 1)) of the block, i.e. of tile (64 WNT wn + 16 j) / 128
+    bf16x8_t bfr[FN];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      bfr[j] = *reinterpret_cast<const bf16x8_t*>(sb + NT * TILE +
-                                                  lds_chunk(wn * 64 + j * 16 + fr, fk / 8));
+    for (int j = 0; j < FN; ++j) {
+      const int row = wn * 64 * WNT + j * 16 + fr;
+      bfr[j] = *reinterpret_cast<const bf16x8_t*>(sb + (NT + row / 128) * TILE +
+                                                  lds_chunk(row % 128, fk / 8));
+    }
 #pragma unroll
     for (int p = 0; p < NT; ++p) {
       bf16x8_t af[4];
@@ -345,7 +374,7 @@ __global__ __launch_bounds__(256) void k_gemm_dma(const bf16_t* __restrict__ A, 
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
   }
@@ -353,11 +382,11 @@ __global__ __launch_bounds__(256) void k_gemm_dma(const bf16_t* __restrict__ A, 
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
-        const int n = n0 + wn * 64 + j * 16 + (lane & 15);
+        const int n = n0 + wn * 64 * WNT + j * 16 + (lane & 15);
         const float v = acc[i][j][r];
         const float o = EPI == GEMV_SWIGLU ? __shfl_xor(v, 1) : 0.f;
         epi_out<EPI>(C, ldc, H, ldh, M, N, m, n, v, o);
@@ -556,14 +585,14 @@ static hipError_t gemm_mfma_launch(const ActBuf& A, int lda, const void* W, int 
   return hipGetLastError();
 }
 
-template <int NT, int EPI, int STG = kDmaStages>
+template <int NT, int EPI, int STG = kDmaStages, int WNT = 1, bool NMAJ = false>
 static hipError_t gemm_dma_launch(const ActBuf& A, int lda, const void* W, int M, int N, int K,
                                   float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st,
                                   int nsplit = 1, size_t c_split = 0) {
-  const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
-  const int grid = (tiles + 7) / 8 * 8;
-  const size_t lds = (size_t)STG * (NT + 1) * 128 * kLDK * sizeof(bf16_t);
-  auto fn = &k_gemm_dma<NT, EPI, STG>;
+  const int n_mt = (M + 127) / 128, n_nt = (N + 128 * WNT - 1) / (128 * WNT);
+  const int grid = NMAJ ? 8 * ((n_nt + 7) / 8) * n_mt : (n_mt * n_nt + 7) / 8 * 8;
+  const size_t lds = (size_t)STG * (NT + WNT) * 128 * kLDK * sizeof(bf16_t);
+  auto fn = &k_gemm_dma<NT, EPI, STG, WNT, NMAJ>;
   if (lds > 65536)
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -645,9 +674,11 @@ static hipError_t gemm_f32(const ActBuf& A, int lda, const WT* W, int M, int N, 
 
 // Split K for products with too few output tiles to fill the chip: as many
 // splits as still leave at most two blocks per CU (512), each at least 256 deep.
+// (bf16 weights: 128 x 256 blocks, see gemm_split_nt; 8-bit weights: 128 x 128.)
 int gemm_split_count(int wt, int nt, int M, int N, int K, int max_split) {
   if (nt < 1 || M <= 32 || (wt != W_BF16 && wt != W_Q8)) return 1;
-  const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  const int bn = wt == W_BF16 ? 256 : 128;
+  const int tiles = ((M + 127) / 128) * ((N + bn - 1) / bn);
   int n = std::max(1, std::min(max_split, 512 / std::max(tiles, 1)));
   while (n > 1 && (K % (kBK * n) || K / n < 256)) --n;
   return n;
@@ -660,7 +691,13 @@ static hipError_t gemm_split_nt(int wt, const ActBuf& A, int lda, const void* W,
   if (wt == W_Q8)
     return gemm_mfma_launch<NT, 2, 2, GEMV_STORE, true>(A, lda, W, M, N, K, P, N, none, 0, st,
                                                          nsplit, p_split);
-  return gemm_dma_launch<NT, GEMV_STORE>(A, lda, W, M, N, K, P, N, none, 0, st, nsplit, p_split);
+  // the residual products (O, down: few output columns, split K): wavefront tiles
+  // of 64 x 128 and each XCD owning a range of weight columns, measured 5-20%
+  // faster than 64 x 64 tiles on the 8B / 32B shapes at 1024 rows (the wider tile
+  // halves the activation fragment reads per product; the placement lets the
+  // row tiles of one weight tile share it in the XCD's L2)
+  return gemm_dma_launch<NT, GEMV_STORE, kDmaStages, 2, true>(A, lda, W, M, N, K, P, N, none, 0,
+                                                              st, nsplit, p_split);
 }
 
 hipError_t launch_gemm_split(int wt, const ActBuf& A, int lda, const void* W, int M, int N, int K,
