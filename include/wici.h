@@ -156,7 +156,10 @@ wici_status wici_load_weights(wici_model* m, const wici_tensor* tensors, int32_t
 /* Append n_tokens prompt ids (host array) at the current position, processing
  * them in chunks of prefill_chunk rows, and return the greedy next token (and,
  * if logits is not NULL, the fp32 logits [vocab] of the last position into host
- * memory).  Synchronous.  Errors: WICI_E_ARG (NULL tokens/first_token,
+ * memory).  Synchronous: the result is final when the call returns (without
+ * logits the call returns as soon as the step's final kernel has published it to
+ * host memory, which may be before the model's stream has retired that kernel;
+ * any later work on the stream is ordered after it).  Errors: WICI_E_ARG (NULL tokens/first_token,
  * n_tokens < 1, an id outside [0, vocab)), WICI_E_STATE (weights incomplete),
  * WICI_E_CAPACITY (position + n_tokens > max_seq), WICI_E_NUMERIC (the
  * positions were still appended; no token is returned, so a following decode
@@ -166,7 +169,8 @@ wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
 
 /* One greedy decode step: feed token_in (or, when token_in < 0, the token the
  * previous prefill/decode call returned) at the current position and return the
- * next token (and optionally the logits, as for wici_prefill).  Synchronous.
+ * next token (and optionally the logits, as for wici_prefill).  Synchronous, as
+ * wici_prefill is.
  * Errors: WICI_E_ARG (NULL next_token, token_in >= vocab), WICI_E_STATE (no
  * prefill since the last reset), WICI_E_CAPACITY, WICI_E_NUMERIC, WICI_E_HIP
  * (also when the attention kernel finds that the blocks of one KV head, which

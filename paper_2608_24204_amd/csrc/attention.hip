@@ -253,8 +253,10 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
   const int Hkv = kv.n_kv;
   int nsplit, split, g;
   if constexpr (FUSE) {
-    // 1-D grid dealt to the XCDs in turn: block b runs on XCD b % 8, and every
-    // split of KV head g is placed on XCD g % 8 (blocks of absent heads exit)
+    // 1-D grid dealt to the XCDs in turn, starting wherever the previous launch
+    // left off (measured: after a one-workgroup launch the next grid's block 0
+    // is not on XCD 0), so blocks with equal b % 8 share an XCD; every split of
+    // KV head g is placed in class g % 8 (blocks of absent heads exit)
     const int b = blockIdx.x, x = b & 7, r = b >> 3, h8 = (Hkv + 7) >> 3;
     g = x + 8 * (r % h8);
     split = r / h8;

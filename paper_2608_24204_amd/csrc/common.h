@@ -138,6 +138,8 @@ struct DecodeState {  // device-resident step state
   int32_t bad;        // nonzero: a logit was NaN/Inf in the last argmax
   int32_t fault;      // nonzero: a decode attention's split blocks of one KV head ran
                       // on different XCDs (see AttnFuse); sticky until reset
+  int32_t done;       // host mirror only: set to 1 by the final argmax kernel after
+                      // the fields above (the host clears it before the step)
 };
 
 }  // namespace wici

@@ -394,9 +394,14 @@ static GemvCfg gemv_cfg(int wt, int epi, int N, int K) {
   c.J = gemv_units(wt, K);
   const int R = gemv_rows(epi, c.J, wt == W_Q8);
   const int ngroups = epi == GEMV_QKV ? N / 2 : (N + R - 1) / R;
-  c.grid = std::max(1, std::min(512, ngroups));
+  // bf16 long-row residual products (K >= 7 x 2048: the FFN down projection) on
+  // 256 double-buffered workgroups: 3.6% faster than 512 in the 8B decode step
+  // (sweep of 256-1024 workgroups, single and double buffering)
+  const bool long_resid = wt == W_BF16 && epi == GEMV_RESID && c.J >= 7;
+  const int g = long_resid ? 256 : 512;
+  c.grid = std::max(1, std::min(g, ngroups));
   c.max_rows = (ngroups + c.grid - 1) / c.grid * R;
-  c.db = c.max_rows / R <= (wt == W_Q8 ? 16 : 8);
+  c.db = c.max_rows / R <= (wt == W_Q8 ? 16 : long_resid ? 16 : 8);
   c.lds = (size_t)4 * c.max_rows * sizeof(float);
   return c;
 }

@@ -330,11 +330,13 @@ __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restr
     st->token = tok;
     st->pos = pos;
     if (pos >= 1) hist[pos - 1] = tok;
-    if (mirror) {  // pinned host copy, read after the stream's synchronisation
+    if (mirror) {  // pinned host copy; `done` last, after a system-scope fence
       mirror->bad = bad;
       mirror->token = tok;
       mirror->pos = pos;
       mirror->fault = st->fault;
+      __threadfence_system();
+      mirror->done = 1;
     }
   }
 }

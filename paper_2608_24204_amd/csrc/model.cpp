@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <algorithm>
+#include <atomic>
 #include <cstring>
 #include <string>
 #include <unordered_map>
@@ -540,13 +541,41 @@ wici_status placement_fault(wici_model* m) {
                              "on one XCD (workgroups not dealt to the XCDs in turn)");
 }
 
+// Clear the mirror's `done` before queueing work whose final argmax writes it.
+void arm_mirror(wici_model* m) {
+  *static_cast<volatile int32_t*>(&m->h_state->done) = 0;
+}
+
+// Wait for the final argmax kernel's `done` in the pinned mirror: a spin on host
+// memory, so the step's result is taken as soon as it lands rather than after
+// the stream's completion has been signalled (on this runtime a wait of a few
+// milliseconds ends in an interrupt-driven sleep, which costs ~15 us per step).
+// The stream is polled as well: if it finishes or fails without `done`, returns
+// false (the caller then synchronises and reports what the stream says).
+bool wait_mirror(wici_model* m) {
+  const volatile int32_t* done = &m->h_state->done;
+  for (uint32_t i = 1;; ++i) {
+    if (*done) {
+      std::atomic_thread_fence(std::memory_order_acquire);
+      return true;
+    }
+    if ((i & 1023) == 0 && hipStreamQuery(m->stream) != hipErrorNotReady) return *done != 0;
+    __builtin_ia32_pause();
+  }
+}
+
 // The step's final argmax kernel has written the new state into the pinned
-// mirror m->h_state as well; it is read once the stream has drained.
+// mirror m->h_state as well.  Without logits to copy, the call returns once the
+// mirror's `done` is set (the stream may still be retiring that kernel; later
+// work on it is ordered after it); otherwise once the stream has drained.
 wici_status finish_step(wici_model* m, int32_t* tok, float* logits) {
-  if (logits)
+  if (logits) {
     HIP_TRY(m, hipMemcpyAsync(logits, m->ds + m->L.logits, (size_t)m->cfg.vocab * 4,
                               hipMemcpyDeviceToHost, m->stream));
-  HIP_TRY(m, hipStreamSynchronize(m->stream));
+    HIP_TRY(m, hipStreamSynchronize(m->stream));
+  } else if (!wait_mirror(m)) {
+    HIP_TRY(m, hipStreamSynchronize(m->stream));
+  }
   m->pos = m->h_state->pos;
   if (m->h_state->fault) return placement_fault(m);
   if (m->h_state->bad) {
@@ -792,6 +821,7 @@ wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
   const Layout& L = m->L;
   const int C = c.prefill_chunk;
   int last_T = 0;
+  arm_mirror(m);
   for (int c0 = 0; c0 < n_tokens; c0 += C) {
     const int T = std::min(C, n_tokens - c0);
     HIP_TRY(m, hipMemcpyAsync(m->ds + L.tokens, tokens + c0, (size_t)T * 4, hipMemcpyHostToDevice,
@@ -823,6 +853,7 @@ wici_status wici_decode_step(wici_model* m, int32_t token_in, int32_t* next_toke
   if (token_in < 0 && !m->have_token) return fail(m, WICI_E_STATE, "no previous token to feed");
   if (m->pos + 1 > m->cfg.max_seq)
     return fail(m, WICI_E_CAPACITY, "position %d reached max_seq", m->pos);
+  arm_mirror(m);
   if (token_in >= 0) HIP_TRY(m, wici::launch_set_token(m->ds + m->L.state, token_in, m->stream));
   HIP_TRY(m, launch_decode_steps(m, 1));
   return finish_step(m, next_token, logits);
@@ -888,6 +919,7 @@ wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* n
   if (token_in < 0 && !m->have_token) return fail(m, WICI_E_STATE, "no previous token to feed");
   if (m->pos + 1 > m->cfg.max_seq)
     return fail(m, WICI_E_CAPACITY, "position %d reached max_seq", m->pos);
+  arm_mirror(m);
   if (token_in >= 0) HIP_TRY(m, wici::launch_set_token(m->ds + m->L.state, token_in, m->stream));
   std::vector<wici::LaunchTimer> tv;
   const hipError_t e = enqueue_decode(m, &tv);
