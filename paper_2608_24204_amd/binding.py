@@ -274,6 +274,10 @@ class WiciModel:
             self._check(self.lib.wici_bind_memory(self.h, self._w.data_ptr(), wb, self._kv.data_ptr(),
                                                   kb, self._s.data_ptr(), sb), "wici_bind_memory")
         self._logits = np.empty(cfg.vocab, np.float32)
+        # per-step call state, built once (the greedy loop calls decode_step per token)
+        self._tok = ctypes.c_int32()
+        self._tok_ref = ctypes.byref(self._tok)
+        self._decode_step_fn = self.lib.wici_decode_step
 
     def _check(self, st: int, what: str, handle="self"):
         if st != WICI_OK:
@@ -331,11 +335,11 @@ class WiciModel:
         return out.value, (self._logits.copy() if want_logits else None)
 
     def decode_step(self, token_in: int = -1, want_logits: bool = False):
-        out = ctypes.c_int32()
         lg = self._logits.ctypes.data if want_logits else None
-        self._check(self.lib.wici_decode_step(self.h, int(token_in), ctypes.byref(out), lg),
-                    "wici_decode_step")
-        return out.value, (self._logits.copy() if want_logits else None)
+        st = self._decode_step_fn(self.h, int(token_in), self._tok_ref, lg)
+        if st != WICI_OK:
+            self._check(st, "wici_decode_step")
+        return self._tok.value, (self._logits.copy() if want_logits else None)
 
     def decode_n(self, n: int, token_in: int = -1, want_logits: bool = False):
         """n greedy decode steps in one call (argmax fed back on the device).

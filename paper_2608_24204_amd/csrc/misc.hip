@@ -293,18 +293,22 @@ hipError_t launch_xor_reduce(const unsigned* in, int n, unsigned* out, hipStream
 }
 
 // ---- argmax, second pass -------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restrict__ part,
-                                                        int n, DecodeState* st,
-                                                        int32_t* __restrict__ hist, int advance,
-                                                        int set_pos, DecodeState* mirror) {
-  __shared__ float sv[16];
-  __shared__ int si[16];
-  __shared__ int sbad[16];
+// One 256-thread workgroup.  The state it updates is read first, alongside the
+// partials, so its load latency is not added after the reduction.
+__global__ __launch_bounds__(256) void k_argmax_final(const ArgmaxPart* __restrict__ part,
+                                                       int n, DecodeState* st,
+                                                       int32_t* __restrict__ hist, int advance,
+                                                       int set_pos, DecodeState* mirror) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  __shared__ int sbad[4];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  DecodeState cur{};
+  if (tid == 0) cur = *st;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
   int bad = 0;
-  for (int i = tid; i < n; i += 1024) {
+  for (int i = tid; i < n; i += 256) {
     const ArgmaxPart p = part[i];
     if (p.i < 0) bad = 1;
     else if (am_better(p.v, p.i, bv, bi)) { bv = p.v; bi = p.i; }
@@ -319,12 +323,12 @@ __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restr
   if (lane == 0) { sv[w] = bv; si[w] = bi; sbad[w] = bad; }
   __syncthreads();
   if (tid == 0) {
-    for (int k = 1; k < 16; ++k) {
+    for (int k = 1; k < 4; ++k) {
       if (am_better(sv[k], si[k], bv, bi)) { bv = sv[k]; bi = si[k]; }
       bad |= sbad[k];
     }
-    if (set_pos < 0 && st->bad) return;  // an earlier step of this run failed
-    const int pos = set_pos >= 0 ? set_pos : st->pos + advance;
+    if (set_pos < 0 && cur.bad) return;  // an earlier step of this run failed
+    const int pos = set_pos >= 0 ? set_pos : cur.pos + advance;
     const int tok = bad ? -1 : bi;
     st->bad = bad;
     st->token = tok;
@@ -334,7 +338,7 @@ __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restr
       mirror->bad = bad;
       mirror->token = tok;
       mirror->pos = pos;
-      mirror->fault = st->fault;
+      mirror->fault = cur.fault;
       __threadfence_system();
       mirror->done = 1;
     }
@@ -343,7 +347,7 @@ __global__ __launch_bounds__(1024) void k_argmax_final(const ArgmaxPart* __restr
 
 hipError_t launch_argmax_final(const ArgmaxPart* part, int n, void* state, int32_t* hist,
                                int advance, int set_pos, void* host_mirror, hipStream_t st) {
-  launch_k(k_argmax_final, dim3(1), dim3(1024), 0, st, kOnly, part, n,
+  launch_k(k_argmax_final, dim3(1), dim3(256), 0, st, kOnly, part, n,
            static_cast<DecodeState*>(state), hist, advance, set_pos,
            static_cast<DecodeState*>(host_mirror));
   return hipGetLastError();
