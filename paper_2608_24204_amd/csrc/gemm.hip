@@ -32,6 +32,14 @@
 namespace wici {
 
 // ------------------------------------------------------------------ epilogue
+// The value of the lane's neighbour across bit 0 of the lane index: in a matrix-core
+// result tile lane l holds column l % 16, so this is the SwiGLU partner (gate 2i,
+// up 2i + 1).  A DPP quad permutation [1, 0, 3, 2] (a register move, where a
+// shuffle goes through the LDS permute unit).
+__device__ __forceinline__ float pair_swap(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+
 template <int EPI>
 __device__ __forceinline__ void epi_out(float* C, int ldc, const ActBuf& H, int ldh, int M,
                                         int N, int m, int n, float v, float other) {
@@ -244,7 +252,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_mfma(
         const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
         const int n = n0 + wn * 64 + j * 16 + (lane & 15);
         const float v = acc[i][j][r];
-        const float o = EPI == GEMV_SWIGLU ? __shfl_xor(v, 1) : 0.f;
+        const float o = EPI == GEMV_SWIGLU ? pair_swap(v) : 0.f;
         epi_out<EPI>(C, ldc, H, ldh, M, N, m, n, v, o);
       }
 }
@@ -280,7 +288,7 @@ __device__ __forceinline__ void wait_vm_lgkm() {
 }
 
 template <int NT, int EPI, int STG = kDmaStages, int WNT = 1, bool NMAJ = false>
-__global__ __launch_bounds__(256) void k_gemm_dma(const bf16_t* __restrict__ A, size_t a_plane,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WNT == 2 ? 2 : 1))) void k_gemm_dma(const bf16_t* __restrict__ A, size_t a_plane,
                                                   int lda, const bf16_t* __restrict__ W, int M,
                                                   int N, int K, int ks, float* __restrict__ C,
                                                   size_t c_split, int ldc, ActBuf H, int ldh) {
@@ -388,7 +396,7 @@ __global__ __launch_bounds__(256) void k_gemm_dma(const bf16_t* __restrict__ A, 
         const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + r;
         const int n = n0 + wn * 64 * WNT + j * 16 + (lane & 15);
         const float v = acc[i][j][r];
-        const float o = EPI == GEMV_SWIGLU ? __shfl_xor(v, 1) : 0.f;
+        const float o = EPI == GEMV_SWIGLU ? pair_swap(v) : 0.f;
         epi_out<EPI>(C, ldc, H, ldh, M, N, m, n, v, o);
       }
 }
@@ -501,7 +509,7 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const bf16_t* __restrict__ 
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = i * 16 + (lane >> 4) * 4 + r, n = n0 + j * 16 + (lane & 15);
-      const float o = EPI == GEMV_SWIGLU ? __shfl_xor(v[r], 1) : 0.f;
+      const float o = EPI == GEMV_SWIGLU ? pair_swap(v[r]) : 0.f;
       epi_out<EPI>(C, ldc, H, ldh, M, N, m, n, v[r], o);
     }
   }
@@ -605,14 +613,31 @@ static hipError_t gemm_dma_launch(const ActBuf& A, int lda, const void* W, int M
 // shapes of 1B-32B models at 1-2K rows, it beats 256 x 128 blocks by 14-35%: the
 // smaller block keeps two workgroups resident per CU, which hides the global-load
 // latency of the next K slice better than the halved weight re-reads save.
+// bf16 weights from 1024 rows on: 64 x 128 wavefront tiles (128 x 256 blocks),
+// each XCD owning a range of weight column tiles.  Measured with two or three
+// activation terms: 8B gate/up 539 -> 504 us at 1024 rows, 32B gate/up 3202 ->
+// 2050 and QKV 528 -> 426 us at 2048 rows; below 1024 rows the halved block
+// count loses (1B QKV at 512 rows 56 -> 87 us, 128-row chunk tails 1.3-1.6x).
+constexpr int kWideRows = 1024;
+
+template <int NT, int EPI>
+static hipError_t gemm_dma_pick(const ActBuf& A, int lda, const void* W, int M, int N, int K,
+                                float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st,
+                                int nsplit = 1, size_t c_split = 0) {
+  if (M >= kWideRows)
+    return gemm_dma_launch<NT, EPI, kDmaStages, 2, true>(A, lda, W, M, N, K, C, ldc, H, ldh, st,
+                                                         nsplit, c_split);
+  return gemm_dma_launch<NT, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st, nsplit, c_split);
+}
+
 template <int EPI, bool Q8>
 static hipError_t gemm_mfma(const ActBuf& A, int lda, const void* W, int M, int N, int K,
                             float* C, int ldc, const ActBuf& H, int ldh, hipStream_t st) {
   if (!Q8) {
     switch (A.nt) {
-      case 1: return gemm_dma_launch<1, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
-      case 2: return gemm_dma_launch<2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
-      case 3: return gemm_dma_launch<3, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+      case 1: return gemm_dma_pick<1, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+      case 2: return gemm_dma_pick<2, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
+      case 3: return gemm_dma_pick<3, EPI>(A, lda, W, M, N, K, C, ldc, H, ldh, st);
       default: return hipErrorInvalidValue;
     }
   }
@@ -674,10 +699,10 @@ static hipError_t gemm_f32(const ActBuf& A, int lda, const WT* W, int M, int N, 
 
 // Split K for products with too few output tiles to fill the chip: as many
 // splits as still leave at most two blocks per CU (512), each at least 256 deep.
-// (bf16 weights: 128 x 256 blocks, see gemm_split_nt; 8-bit weights: 128 x 128.)
+// (Blocks of 128 x 256 for bf16 weights from kWideRows rows on, else 128 x 128.)
 int gemm_split_count(int wt, int nt, int M, int N, int K, int max_split) {
   if (nt < 1 || M <= 32 || (wt != W_BF16 && wt != W_Q8)) return 1;
-  const int bn = wt == W_BF16 ? 256 : 128;
+  const int bn = wt == W_BF16 && M >= kWideRows ? 256 : 128;
   const int tiles = ((M + 127) / 128) * ((N + bn - 1) / bn);
   int n = std::max(1, std::min(max_split, 512 / std::max(tiles, 1)));
   while (n > 1 && (K % (kBK * n) || K / n < 256)) --n;
@@ -691,13 +716,11 @@ static hipError_t gemm_split_nt(int wt, const ActBuf& A, int lda, const void* W,
   if (wt == W_Q8)
     return gemm_mfma_launch<NT, 2, 2, GEMV_STORE, true>(A, lda, W, M, N, K, P, N, none, 0, st,
                                                          nsplit, p_split);
-  // the residual products (O, down: few output columns, split K): wavefront tiles
-  // of 64 x 128 and each XCD owning a range of weight columns, measured 5-20%
-  // faster than 64 x 64 tiles on the 8B / 32B shapes at 1024 rows (the wider tile
-  // halves the activation fragment reads per product; the placement lets the
-  // row tiles of one weight tile share it in the XCD's L2)
-  return gemm_dma_launch<NT, GEMV_STORE, kDmaStages, 2, true>(A, lda, W, M, N, K, P, N, none, 0,
-                                                              st, nsplit, p_split);
+  // the residual products (O, down: few output columns, split K) from 1024 rows
+  // on: 8B down 274 -> 235 us, O 70 -> 66 us (the wider tile halves the
+  // activation fragment reads per product; the placement lets the row tiles of
+  // one weight tile share it in the XCD's L2)
+  return gemm_dma_pick<NT, GEMV_STORE>(A, lda, W, M, N, K, P, N, none, 0, st, nsplit, p_split);
 }
 
 hipError_t launch_gemm_split(int wt, const ActBuf& A, int lda, const void* W, int M, int N, int K,

@@ -372,9 +372,12 @@ __global__ __launch_bounds__(256) void k_gemv(const WT* __restrict__ W, int N, i
 // per CU; a workgroup with at most 8 groups (16 for Q8) double-buffers them
 // when the two buffers fit the registers (its groups' round trips would otherwise follow one
 // another), one with more groups streams them one at a time (double buffering
-// there puts too many bytes in flight).  (From
-// sweeps of 256..1536 workgroups and single or double buffering over the
-// decode matrices of the 8B shape.)
+// there puts too many bytes in flight) — except bf16 rows of three units
+// (K = 4097..6144, the 32B shape's K = 5120), which stream at ~4.4 TB/s single
+// buffered and ~6.8 double buffered whatever the group count (gate/up 127 ->
+// 83 us, LM head 344 -> 229 us at 512 workgroups).  (From sweeps of 256..1536
+// workgroups and single or double buffering over the decode matrices of the 8B
+// and 32B shapes.)
 struct GemvCfg {
   int J, grid, max_rows;
   bool db;  // double-buffered groups (few groups per workgroup)
@@ -401,7 +404,8 @@ static GemvCfg gemv_cfg(int wt, int epi, int N, int K) {
   const int g = long_resid ? 256 : 512;
   c.grid = std::max(1, std::min(g, ngroups));
   c.max_rows = (ngroups + c.grid - 1) / c.grid * R;
-  c.db = c.max_rows / R <= (wt == W_Q8 ? 16 : long_resid ? 16 : 8);
+  c.db = c.max_rows / R <= (wt == W_Q8 ? 16 : long_resid ? 16 : 8) ||
+         (wt == W_BF16 && c.J == 3);
   c.lds = (size_t)4 * c.max_rows * sizeof(float);
   return c;
 }

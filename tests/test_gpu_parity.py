@@ -192,10 +192,17 @@ def test_kv_cache_holds_oracle_values(cuda_ok):
                 assert not viol.any(), (np.argwhere(viol)[:5], g[viol][:5], o[viol][:5])
                 assert np.mean(g != o) < 0.01
             else:
-                # deeper layers also carry the one-step differences of the cache
-                # below them through attention: compare at the logit tolerance scale
-                # (one storage step plus the propagated error)
-                assert np.all(np.abs(g - o) <= np.abs(o) * 2.0 ** -7 + 2e-3 * scale)
+                # deeper layers: the input already differs from the oracle's by the
+                # float32 error of the layers below (and through attention by the
+                # one-step storage differences of the cache below), a relative
+                # error of order 2^-20 here.  Both sides then round to bf16, so
+                # the results are at most one storage step apart plus that input
+                # error; the bound allows 2^-14 of max|o| for it (measured worst:
+                # 1.5e-6 = 2^-19.3 of max|o| beyond one step, on 0.46% of entries)
+                bound = np.abs(o) * 2.0 ** -7 + scale * 2.0 ** -14
+                viol = np.abs(g - o) > bound
+                assert not viol.any(), (l, np.argwhere(viol)[:5], g[viol][:5], o[viol][:5])
+                assert np.mean(g != o) < 0.02
                 assert np.mean(g != o) < 0.2
 
 
