@@ -155,9 +155,13 @@ hipError_t launch_attn_decode_batch(bool kv_bf16, const float* q, int q_stride, 
 
 // Prefill: rotate q (in place) and k of T rows at positions p0..p0+T-1 and
 // append k, v to the cache.  qkv rows are [Hq*hd | Hkv*hd | Hkv*hd] fp32.
+// nsplit > 1: the projection was split along K and its rows are the sums, in
+// range order, of the nsplit partial products part[s * p_split + ...] (same row
+// layout); the rotated queries are then written to qkv.
 hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
                               const float* cos_t, const float* sin_t, KvLayout kv,
-                              hipStream_t st);
+                              hipStream_t st, const float* part = nullptr, int nsplit = 1,
+                              size_t p_split = 0);
 
 // Prefill attention: queries = rotated q rows of qkv (T rows at p0..), keys =
 // cache positions [0, p0+T), causal; out [T, Hq*hd] (row stride Hq*hd).

@@ -196,24 +196,32 @@ template <typename KT>
 __global__ __launch_bounds__(256) void k_rope_append(float* __restrict__ qkv, int p0, int Hq,
                                                      const float* __restrict__ cos_t,
                                                      const float* __restrict__ sin_t,
-                                                     KvLayout kv) {
+                                                     KvLayout kv, const float* __restrict__ part,
+                                                     int nsplit, size_t p_split) {
   const int t = blockIdx.x, pos = p0 + t;
   const int hd = kv.hd, half = hd >> 1, Hkv = kv.n_kv;
   const int width = (Hq + 2 * Hkv) * hd;
   float* row = qkv + (size_t)t * width;
+  // element i of the row: the projection's output, or the sum of its K-range
+  // partial products in range order
+  const float* prow = part ? part + (size_t)t * width : row;
+  auto val = [&](int i) {
+    float v = prow[i];
+    for (int s = 1; s < nsplit; ++s) v += prow[(size_t)s * p_split + i];
+    return v;
+  };
   const float* cr = cos_t + (size_t)pos * half;
   const float* sr = sin_t + (size_t)pos * half;
   KT* base = static_cast<KT*>(kv.base);
   const int phys = kv.table[pos / kv.page], slot = pos % kv.page;
-  // rotate q heads in place, k heads into the cache
+  // rotate q heads (into qkv), k heads into the cache
   for (int i = threadIdx.x; i < (Hq + Hkv) * half; i += blockDim.x) {
     const int h = i / half, j = i % half;
-    float* z = row + h * hd;
-    const float a = z[j], b = z[j + half], c = cr[j], s = sr[j];
+    const float a = val(h * hd + j), b = val(h * hd + j + half), c = cr[j], s = sr[j];
     const float ra = a * c - b * s, rb = a * s + b * c;
     if (h < Hq) {
-      z[j] = ra;
-      z[j + half] = rb;
+      row[h * hd + j] = ra;
+      row[h * hd + j + half] = rb;
     } else {
       const int g = h - Hq;
       KT* dst = base + (((size_t)phys * 2 + 0) * Hkv + g) * kv.page * hd + (size_t)slot * hd;
@@ -224,19 +232,21 @@ __global__ __launch_bounds__(256) void k_rope_append(float* __restrict__ qkv, in
   for (int i = threadIdx.x; i < Hkv * hd; i += blockDim.x) {
     const int g = i / hd, e = i % hd;
     KT* dst = base + (((size_t)phys * 2 + 1) * Hkv + g) * kv.page * hd + (size_t)slot * hd;
-    Elem<KT>::store(dst + e, row[(Hq + Hkv) * hd + i]);
+    Elem<KT>::store(dst + e, val((Hq + Hkv) * hd + i));
   }
 }
 
 hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
                               const float* cos_t, const float* sin_t, KvLayout kv,
-                              hipStream_t st) {
+                              hipStream_t st, const float* part, int nsplit, size_t p_split) {
+  if (nsplit < 1 || (nsplit > 1 && !part)) return hipErrorInvalidValue;
+  if (nsplit == 1) part = nullptr;
   if (kv_bf16)
     hipLaunchKernelGGL(k_rope_append<bf16_t>, dim3(T), dim3(256), 0, st, qkv, p0, Hq, cos_t,
-                       sin_t, kv);
+                       sin_t, kv, part, nsplit, p_split);
   else
     hipLaunchKernelGGL(k_rope_append<float>, dim3(T), dim3(256), 0, st, qkv, p0, Hq, cos_t,
-                       sin_t, kv);
+                       sin_t, kv, part, nsplit, p_split);
   return hipGetLastError();
 }
 
