@@ -66,12 +66,11 @@ typedef enum {
   WICI_PREFILL_BF16X3 = 3, /* matrix cores, bf16; three bf16 terms per activation
                               (three products per tile), fp32-accurate */
   WICI_PREFILL_BF16X3Q = 4 /* matrix cores, bf16; three bf16 terms stored, the Q/K/V
-                              projection reads all three and the O, gate/up and down
-                              projections the first two (the cached keys and values
-                              carry the prompt's precision into every decode step;
-                              the other products' ~2^-16 leaves the workloads'
-                              greedy ids unchanged, measured), 18-26% less prefill
-                              time than BF16X3 */
+                              projection and the attention read all three and the
+                              O, gate/up and down projections the first two (the
+                              cached keys and values carry the prompt's precision
+                              into every decode step; the other products' ~2^-16
+                              leaves the workloads' greedy ids unchanged, measured) */
 } wici_prefill_mode;
 
 enum { WICI_FLAG_NO_GRAPH = 1 }; /* run decode steps eagerly instead of replaying a graph */
@@ -98,9 +97,11 @@ typedef struct {
                              prefill_mode says.  Else (WICI_PREFILL_BF16X3 only)
                              the number of the three bf16 terms each product reads,
                              two bits each (1..3): bits 0-1 the Q/K/V projection,
-                             2-3 the O projection, 4-5 gate/up, 6-7 down; a product
-                             reading fewer terms does less matrix work and carries
-                             its activations to ~2^-16 (two) or ~2^-8 (one) */
+                             2-3 the O projection, 4-5 gate/up, 6-7 down, and bits
+                             8-9 the terms of the attention's query and
+                             probabilities (0: three); a product reading fewer
+                             terms does less matrix work and carries its
+                             activations to ~2^-16 (two) or ~2^-8 (one) */
 } wici_config;
 
 /* One named weight tensor in logical [out, in] row-major layout.  Names:

@@ -112,7 +112,8 @@ def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool =
                 max_seq: int | None = None, prefill_chunk: int | None = None,
                 kv_page: int | None = None, prefill_planes=None) -> WiciConfig:
     """prefill_planes: None/0 for prefill_mode's own term count, or a tuple
-    (qkv, o, gate_up, down) of bf16 terms each projection reads (bf16x3 only)."""
+    (qkv, o, gate_up, down[, attention]) of bf16 terms each projection reads and
+    the prefill attention carries (bf16x3 only; attention defaults to three)."""
     if prefill_mode is None:
         prefill_mode = "f32" if cfg.weight_dtype == "f32" else "bf16x3q"
     c = WiciConfig()
@@ -128,8 +129,8 @@ def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool =
     c.prefill_mode = PREFILL_MODES[prefill_mode]
     c.flags = 0 if graph else WICI_FLAG_NO_GRAPH
     if prefill_planes:
-        q, o, gu, dn = prefill_planes
-        c.prefill_planes = q | (o << 2) | (gu << 4) | (dn << 6)
+        q, o, gu, dn, *at = prefill_planes
+        c.prefill_planes = q | (o << 2) | (gu << 4) | (dn << 6) | ((at[0] if at else 0) << 8)
     return c
 
 

@@ -840,9 +840,9 @@ static hipError_t attn_prefill_t(const float* qkv, int T, int p0, int Hq, KvLayo
 
 template <int HD>
 static hipError_t attn_prefill_mfma(const float* qkv, int T, int p0, int Hq, KvLayout kv,
-                                    const ActBuf& out, hipStream_t s) {
+                                    const ActBuf& out, int terms, hipStream_t s) {
   const dim3 grid((T + 63) / 64, Hq);
-  switch (out.nt) {
+  switch (terms) {
     case 1: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 1>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
     case 2: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 2>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
     case 3: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 3>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
@@ -852,14 +852,16 @@ static hipError_t attn_prefill_mfma(const float* qkv, int T, int p0, int Hq, KvL
 }
 
 // bf16 cache with split-activation output: matrix cores, with the query and the
-// probabilities carried in as many bf16 terms as the output; otherwise the fp32
-// vector kernel.
+// probabilities carried in `terms` bf16 terms (0: as many as the output stores);
+// otherwise the fp32 vector kernel.
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
-                               KvLayout kv, const ActBuf& out, hipStream_t s) {
-  if (kv.page < 1 || (kv.page & (kv.page - 1))) return hipErrorInvalidValue;
+                               KvLayout kv, const ActBuf& out, hipStream_t s, int terms) {
+  if (kv.page < 1 || (kv.page & (kv.page - 1)) || terms < 0 || terms > 3)
+    return hipErrorInvalidValue;
   if (kv_bf16 && out.nt >= 1) {
-    if (kv.hd == 128) return attn_prefill_mfma<128>(qkv, T, p0, Hq, kv, out, s);
-    if (kv.hd == 64) return attn_prefill_mfma<64>(qkv, T, p0, Hq, kv, out, s);
+    const int nt = terms > 0 ? terms : out.nt;
+    if (kv.hd == 128) return attn_prefill_mfma<128>(qkv, T, p0, Hq, kv, out, nt, s);
+    if (kv.hd == 64) return attn_prefill_mfma<64>(qkv, T, p0, Hq, kv, out, nt, s);
     return hipErrorInvalidValue;
   }
   if (kv.hd == 128) {

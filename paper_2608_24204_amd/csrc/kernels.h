@@ -164,9 +164,12 @@ hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
                               size_t p_split = 0);
 
 // Prefill attention: queries = rotated q rows of qkv (T rows at p0..), keys =
-// cache positions [0, p0+T), causal; out [T, Hq*hd] (row stride Hq*hd).
+// cache positions [0, p0+T), causal; out [T, Hq*hd] (row stride Hq*hd).  With a
+// bf16 cache and split output, the scores and probabilities go through the matrix
+// cores with the query and the probabilities as `terms` bf16 terms (1-3; 0: as
+// many as `out` stores).
 hipError_t launch_attn_prefill(bool kv_bf16, const float* qkv, int T, int p0, int Hq,
-                               KvLayout kv, const ActBuf& out, hipStream_t st);
+                               KvLayout kv, const ActBuf& out, hipStream_t st, int terms = 0);
 
 
 // Decode attention at position state->pos: q = the rotated, pre-scaled queries

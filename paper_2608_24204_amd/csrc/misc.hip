@@ -181,12 +181,82 @@ __global__ __launch_bounds__(256) void k_resid_sum_rmsnorm(float* __restrict__ x
   }
 }
 
+// The same for rows of NV * 1024 values and NS partials: every load of the row
+// (x, the partials, the gain) is issued at once and the row stays in registers for
+// the norm (the loop form above waits for each partial in turn and reads x
+// back).  Same elements per thread and the same order of additions, so the
+// results are bit-identical.  8B at 1024 rows, four partials: 25.6 -> ~17 us.
+template <int NS, int NV>
+__global__ __launch_bounds__(256) void k_resid_sum_rmsnorm_reg(float* __restrict__ x,
+                                                               const float* __restrict__ P,
+                                                               size_t p_split,
+                                                               const float* __restrict__ g,
+                                                               float eps, int d, ActBuf y) {
+  __shared__ float red[4];
+  float4* xr = reinterpret_cast<float4*>(x + (size_t)blockIdx.x * d);
+  const float4* pr = reinterpret_cast<const float4*>(P + (size_t)blockIdx.x * d);
+  const size_t yr = (size_t)blockIdx.x * d;
+  const int tid = threadIdx.x;
+  float4 v[NV], p[NS][NV], w[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = xr[tid + 256 * i];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int i = 0; i < NV; ++i) p[s][i] = pr[s * (p_split / 4) + tid + 256 * i];
+  if (g) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) w[i] = reinterpret_cast<const float4*>(g)[tid + 256 * i];
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      v[i].x += p[s][i].x; v[i].y += p[s][i].y; v[i].z += p[s][i].z; v[i].w += p[s][i].w;
+    }
+    xr[tid + 256 * i] = v[i];
+    ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+  }
+  if (!g) return;
+  const float r = 1.0f / sqrtf(block256_sum(ss, red) / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const size_t k = yr + 4 * (tid + 256 * i);
+    store_act(y, k + 0, v[i].x * r * w[i].x);
+    store_act(y, k + 1, v[i].y * r * w[i].y);
+    store_act(y, k + 2, v[i].z * r * w[i].z);
+    store_act(y, k + 3, v[i].w * r * w[i].w);
+  }
+}
+
+template <int NS>
+static bool resid_sum_reg(float* x, const float* P, size_t p_split, const float* gain, float eps,
+                          int T, int d, const ActBuf& y, hipStream_t st) {
+  if (d % 1024 || p_split % 4) return false;
+  switch (d / 1024) {
+#define WICI_RS(NV)                                                                           \
+  case NV:                                                                                    \
+    hipLaunchKernelGGL((k_resid_sum_rmsnorm_reg<NS, NV>), dim3(T), dim3(256), 0, st, x, P, \
+                       p_split, gain, eps, d, y);                                             \
+    return true;
+    WICI_RS(1) WICI_RS(2) WICI_RS(3) WICI_RS(4) WICI_RS(5) WICI_RS(6) WICI_RS(7) WICI_RS(8)
+#undef WICI_RS
+    default: return false;
+  }
+}
+
 hipError_t launch_resid_sum_rmsnorm(float* x, const float* P, int nsplit, size_t p_split,
                                     const float* gain, float eps, int T, int d, const ActBuf& y,
                                     hipStream_t st) {
   if (nsplit < 1 || d % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_resid_sum_rmsnorm, dim3(T), dim3(256), 0, st, x, P, nsplit, p_split, gain,
-                     eps, d, y);
+  const bool reg = nsplit == 2   ? resid_sum_reg<2>(x, P, p_split, gain, eps, T, d, y, st)
+                   : nsplit == 3 ? resid_sum_reg<3>(x, P, p_split, gain, eps, T, d, y, st)
+                   : nsplit == 4 ? resid_sum_reg<4>(x, P, p_split, gain, eps, T, d, y, st)
+                                 : false;
+  if (!reg)
+    hipLaunchKernelGGL(k_resid_sum_rmsnorm, dim3(T), dim3(256), 0, st, x, P, nsplit, p_split,
+                       gain, eps, d, y);
   return hipGetLastError();
 }
 

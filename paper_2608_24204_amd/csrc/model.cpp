@@ -34,21 +34,25 @@ constexpr int kMaxKSplit = 4;   // K ranges of a prefill residual product (parti
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 size_t dsize(int32_t dt) { return dt == WICI_BF16 ? 2 : 4; }
 
-// bf16 activation terms stored for the prefill products, and read by each of them
+// bf16 activation terms stored for the prefill products, read by each of them,
+// and carried by the prefill attention's query and probabilities
 struct Planes {
-  int store, qkv, o, gu, down;
+  int store, qkv, o, gu, down, attn;
 };
 Planes prefill_planes(const wici_config& c) {
   const int nt = c.prefill_mode == WICI_PREFILL_F32 ? 0
                  : c.prefill_mode == WICI_PREFILL_BF16 ? 1
                  : c.prefill_mode == WICI_PREFILL_BF16X2 ? 2 : 3;
-  Planes p{nt, nt, nt, nt, nt};
-  if (c.prefill_mode == WICI_PREFILL_BF16X3Q) p = Planes{3, 3, 2, 2, 2};
+  Planes p{nt, nt, nt, nt, nt, nt};
+  // (two attention terms flip the 8B shape's 8-bit run at a near tie: three stay)
+  if (c.prefill_mode == WICI_PREFILL_BF16X3Q) p = Planes{3, 3, 2, 2, 2, 3};
   if (c.prefill_planes) {
     p.qkv = c.prefill_planes & 3;
     p.o = (c.prefill_planes >> 2) & 3;
     p.gu = (c.prefill_planes >> 4) & 3;
     p.down = (c.prefill_planes >> 6) & 3;
+    const int at = (c.prefill_planes >> 8) & 3;
+    p.attn = at ? at : nt;
   }
   return p;
 }
@@ -105,7 +109,7 @@ bool config_ok(const wici_config* c, std::string* why) {
   if (c->prefill_planes != 0) {
     if (c->prefill_mode != WICI_PREFILL_BF16X3)
       return bad("prefill_planes needs prefill_mode WICI_PREFILL_BF16X3");
-    if (c->prefill_planes & ~0xff) return bad("prefill_planes has bits above 7");
+    if (c->prefill_planes & ~0x3ff) return bad("prefill_planes has bits above 9");
     for (int i = 0; i < 4; ++i)
       if (((c->prefill_planes >> (2 * i)) & 3) == 0) return bad("prefill_planes: a field of 0");
   }
@@ -435,7 +439,8 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
                                       m->W<float>(L.rope_sin), m->kv(l), s, s_q > 1 ? P : nullptr,
                                       s_q, q_split)))
       return e;
-    if ((e = wici::launch_attn_prefill(kb, qkv, T, p0, c.n_heads, m->kv(l), att, s))) return e;
+    if ((e = wici::launch_attn_prefill(kb, qkv, T, p0, c.n_heads, m->kv(l), att, s, pl.attn)))
+      return e;
     if ((e = resid(rd(att, pl.o), qd, m->layer(l, L.l_wo), s_o))) return e;
     if ((e = norm(m->W<float>(m->layer(l, L.l_fnorm)), s_o))) return e;
     if ((e = wici::launch_gemm(wb, wici::GEMV_SWIGLU, rd(a, pl.gu), d,

@@ -63,11 +63,13 @@ def test_invalid_config_is_rejected(field, value):
 
 @pytest.mark.parametrize("mode,planes,ok", [
     ("bf16x3", 0x9e, True), ("bf16x3", 0xff, True), ("bf16x3", 0x55, True),
-    ("bf16x3", 0x9c, False), ("bf16x3", 0x1ff, False), ("bf16x3q", 0x9e, False),
+    ("bf16x3", 0x9c, False), ("bf16x3", 0x29e, True), ("bf16x3", 0x455, False),
+    ("bf16x3q", 0x9e, False),
     ("bf16x2", 0x55, False)])
 def test_prefill_planes_field(mode, planes, ok):
-    """Two bits per product (Q/K/V, O, gate/up, down), each 1..3, and only with
-    the three-term mode that stores all of them."""
+    """Two bits per product (Q/K/V, O, gate/up, down), each 1..3, two more for
+    the attention's terms (0 = three), and only with the three-term mode that
+    stores all of them."""
     lib = binding.load_library()
     c = _cfg(weight_dtype="bf16", kv_dtype="bf16")
     c.prefill_mode = binding.PREFILL_MODES[mode]
@@ -81,6 +83,9 @@ def test_prefill_planes_field(mode, planes, ok):
 def test_make_config_packs_plane_fields():
     c = binding.make_config(configs.CONFIGS["1b"], prefill_mode="bf16x3", prefill_planes=(3, 2, 1, 2))
     assert c.prefill_planes == 3 | 2 << 2 | 1 << 4 | 2 << 6
+    c = binding.make_config(configs.CONFIGS["1b"], prefill_mode="bf16x3",
+                            prefill_planes=(3, 2, 2, 2, 2))
+    assert c.prefill_planes == 3 | 2 << 2 | 2 << 4 | 2 << 6 | 2 << 8
     assert binding.make_config(configs.CONFIGS["1b"]).prefill_mode == binding.PREFILL_MODES["bf16x3q"]
 
 

@@ -145,11 +145,12 @@ def _prefill_logits(cfg, w, prompt, n, **kw):
     return ids, np.stack(logs)
 
 
-@pytest.mark.parametrize("planes,same_as", [((3, 2, 2, 2), "bf16x3q"), ((3, 3, 3, 3), "bf16x3")])
+@pytest.mark.parametrize("planes,same_as", [((3, 2, 2, 2), "bf16x3q"), ((3, 2, 2, 2, 3), "bf16x3q"),
+                                            ((3, 3, 3, 3), "bf16x3")])
 def test_prefill_plane_fields_match_whole_modes(cuda_ok, planes, same_as):
-    """Both modes store three bf16 terms (so prefill attention carries its query
-    and probabilities in three terms alike); the per-product fields then choose
-    exactly the terms each product of the whole mode reads, bit for bit."""
+    """Both modes store three bf16 terms; the per-product fields then choose
+    exactly the terms each product of the whole mode reads, and the attention's
+    query and probability terms (three when the field is left out), bit for bit."""
     cfg = SMALL["gqa128_bf16"]
     w, _ = weights_for(cfg, 0.1)
     prompt = inputs.make_prompt(cfg, 150)
@@ -157,6 +158,17 @@ def test_prefill_plane_fields_match_whole_modes(cuda_ok, planes, same_as):
     b = _prefill_logits(cfg, w, prompt, 3, prefill_mode=same_as)
     assert a[0] == b[0]
     assert np.array_equal(a[1], b[1])
+
+
+def test_prefill_attention_with_two_terms(cuda_ok):
+    """The attention field of prefill_planes: query and probabilities as two bf16
+    terms (the default keeps three) against the oracle."""
+    cfg = SMALL["gqa128_bf16"]
+    prompt = inputs.make_prompt(cfg, 150)
+    rep, _, _ = run_parity(cfg, prompt, 6, gain_std=0.1, prefill_mode="bf16x3",
+                           prefill_planes=(3, 2, 2, 2, 2), max_seq=160)
+    assert rep.max_rel_err <= 1e-3
+    assert rep.strict_ids, rep.summary()
 
 
 def test_kv_cache_holds_oracle_values(cuda_ok):
