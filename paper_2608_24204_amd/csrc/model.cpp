@@ -164,7 +164,8 @@ Layout make_layout(const wici_config& c) {
   L.parts = o; o = align_up(o + kMaxGemvBlocks * sizeof(ArgmaxPart));
   L.part_o = o; o = align_up(o + (size_t)c.n_heads * L.nsplit * c.head_dim * 4);
   L.part_ml = o; o = align_up(o + (size_t)c.n_heads * L.nsplit * 2 * 4);
-  L.tokens = o; o = align_up(o + C * 4);
+  // token ids: a whole prompt (copied once per prefill call), or a batch's tokens
+  L.tokens = o; o = align_up(o + (size_t)std::max<int64_t>(C, std::max(c.max_seq, kMaxBatch)) * 4);
   L.table = o; o = align_up(o + (size_t)L.n_pages * 4);
   L.state = o; o = align_up(o + sizeof(DecodeState));
   L.hist = o; o = align_up(o + (size_t)c.max_seq * 4);  // token emitted after each position
@@ -367,7 +368,7 @@ hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers 
 
 // Enqueue one prefill chunk of T rows at positions p0.. (token ids already on
 // the device); x[T-1] holds the last row's residual stream afterwards.
-hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
+hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T, int tok_off) {
   const wici_config& c = m->cfg;
   const Layout& L = m->L;
   const int wb = c.weight_dtype;
@@ -396,8 +397,8 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T) {
   const wici::ActBuf none{};
   hipStream_t s = m->stream;
   hipError_t e;
-  if ((e = wici::launch_embed(wb, m->dw + L.embed, c.vocab, d, m->S<int32_t>(L.tokens), T, nullptr,
-                              x, s)))
+  if ((e = wici::launch_embed(wb, m->dw + L.embed, c.vocab, d, m->S<int32_t>(L.tokens) + tok_off,
+                              T, nullptr, x, s)))
     return e;
   // The residual products (O, down) have only d output columns: with few rows
   // they are split along K into partials that the next row RMSNorm adds to x
@@ -840,13 +841,13 @@ wici_status wici_prefill(wici_model* m, const int32_t* tokens, int32_t n_tokens,
   const int C = c.prefill_chunk;
   int last_T = 0;
   arm_mirror(m);
+  // every chunk's ids in one copy (the buffer holds max_seq ids), so the chunks
+  // queue back to back with no host wait between them
+  HIP_TRY(m, hipMemcpyAsync(m->ds + L.tokens, tokens, (size_t)n_tokens * 4, hipMemcpyHostToDevice,
+                            m->stream));
   for (int c0 = 0; c0 < n_tokens; c0 += C) {
     const int T = std::min(C, n_tokens - c0);
-    HIP_TRY(m, hipMemcpyAsync(m->ds + L.tokens, tokens + c0, (size_t)T * 4, hipMemcpyHostToDevice,
-                              m->stream));
-    HIP_TRY(m, enqueue_prefill_chunk(m, m->pos + c0, T));
-    // the token buffer is reused by the next chunk: wait for this one
-    if (c0 + C < n_tokens) HIP_TRY(m, hipStreamSynchronize(m->stream));
+    HIP_TRY(m, enqueue_prefill_chunk(m, m->pos + c0, T, c0));
     last_T = T;
   }
   int nb = 0;
