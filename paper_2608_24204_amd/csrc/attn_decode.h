@@ -12,7 +12,6 @@ constexpr int kChunk = 64;       // positions per decode split (at most one per 
 
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
 // Merge of a KV head's splits in the last of its split blocks to finish (the
 // batch-1 launch of k_attn_decode_mfma with FUSE, at most kFuseMaxSplits splits).
@@ -29,18 +28,6 @@ typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 // reports as an error.
 constexpr int kFuseMaxSplits = 32;
 constexpr int kFuseLine = 64;   // ints per head of the counter and XCD arrays (256 bytes)
-
-__device__ __forceinline__ int xcc_id() {
-  return (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 0xf);
-}
-
-// 16 bytes at byte offset `off` of the buffer `r`, read past the L1 (sc0).
-__device__ __forceinline__ u32x4_t load_l2(__amdgpu_buffer_rsrc_t r, int off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 1);
-}
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, size_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
-}
 
 template <int HD, int G>
 __device__ __forceinline__ void attn_merge_in_last_split(const AttnFuse& fz, int g, int split,

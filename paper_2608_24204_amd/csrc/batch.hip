@@ -85,10 +85,21 @@ __global__ __launch_bounds__(1024) void k_argmax_rows(const float* __restrict__ 
   float bv = -INFINITY;
   int bi = 0x7fffffff;
   int bad = 0;
-  for (int i = tid; i < V; i += 1024) {
-    const float v = row[i];
-    bad |= !isfinite(v);
-    if (am_better(v, i, bv, bi)) { bv = v; bi = i; }
+  // eight loads in flight per thread (one at a time the row's 500 KB took ~47 us
+  // of load latency); the comparison picks the same element in any order
+  constexpr int U = 8;
+  for (int i0 = tid; i0 < V; i0 += 1024 * U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = row[min(i0 + 1024 * u, V - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + 1024 * u;
+      if (i < V) {
+        bad |= !isfinite(v[u]);
+        if (am_better(v[u], i, bv, bi)) { bv = v[u]; bi = i; }
+      }
+    }
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {

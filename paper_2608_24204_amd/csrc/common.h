@@ -136,10 +136,27 @@ struct DecodeState {  // device-resident step state
   int32_t pos;        // number of cached positions
   int32_t token;      // last emitted (or host-given) token
   int32_t bad;        // nonzero: a logit was NaN/Inf in the last argmax
-  int32_t fault;      // nonzero: a decode attention's split blocks of one KV head ran
-                      // on different XCDs (see AttnFuse); sticky until reset
+  int32_t fault;      // nonzero: the split blocks of an in-launch merge (a decode
+                      // attention's KV head, a batched product's tile) ran on
+                      // different XCDs; sticky until reset
   int32_t done;       // host mirror only: set to 1 by the final argmax kernel after
                       // the fields above (the host clears it before the step)
 };
+
+// ---- exchange between the workgroups of one XCD (in-launch merges) ----------
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// The XCC (XCD) the wavefront runs on: hardware register XCC_ID, bits 0-3.
+__device__ __forceinline__ int xcc_id() {
+  return (int)(__builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 0xf);
+}
+
+// 16 bytes at byte offset `off` of the buffer `r`, read past the L1 (sc0).
+__device__ __forceinline__ u32x4_t load_l2(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 1);
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)bytes, 0x00020000);
+}
 
 }  // namespace wici

@@ -515,6 +515,166 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const bf16_t* __restrict__ 
   }
 }
 
+// ------------------------------------------------- few rows, staged through LDS
+// The same product for at most 32 rows, bf16 weights, K a multiple of 128: a
+// workgroup owns 64 weight rows (16 per wavefront) and walks its K range in
+// 128-deep slices through a ring of kRowsStages LDS stages, the weight slice
+// (64 rows x 256 bytes) and the activation slice (NT planes x 16 TM rows x 256
+// bytes) fetched by global_load_lds_dwordx4 in whole 128-byte lines, sixteen
+// lanes to a row.  (Fragment-shaped loads straight into registers touch sixteen
+// rows per instruction, 64 bytes each, and stream no faster than ~4.9 TB/s.)
+// The sixteen 16-byte chunks of a row are XOR-swizzled by the row's low four
+// bits, so a fragment read (sixteen rows, one chunk) covers all 64 banks once.
+//
+// Products with few weight rows are split along K over grid slots: the splits
+// of a 64-row tile occupy workgroup indices of one residue mod 8, so they run on
+// one XCD (dispatch deals workgroups to the XCDs in turn) and exchange their
+// partials through its L2, as the decode attention merge does: each split
+// stores its accumulators, waits for the L2 to acknowledge them, records its
+// XCD and takes a ticket from the tile's counter; the last one drops its CU's
+// L1, adds the partials in split order (so the sum does not depend on timing),
+// applies the epilogue and resets the counter.  A split that ran elsewhere
+// sets *fault.
+constexpr int kRowsKC = 128;     // K per LDS stage
+constexpr int kRowsStages = 3;   // two slices in flight while one is multiplied
+static_assert(kRowsStages >= 2 && kRowsStages <= 4, "stage ring of 2-4");
+constexpr int kRowsSyncLine = 64;  // ints per tile: counter at 0, XCD records from 32
+constexpr int kRowsMaxTiles = kGemmRowsSyncInts / kRowsSyncLine;  // tiles that can be split
+
+template <int NT, int TM, int EPI>
+__global__ __launch_bounds__(256) void k_gemm_rows(const bf16_t* __restrict__ A, size_t a_plane,
+                                                   int lda, const bf16_t* __restrict__ W, int M,
+                                                   int N, int K, int nsplit, int ks,
+                                                   float* __restrict__ C, int ldc, ActBuf H,
+                                                   int ldh, floatx4_t* __restrict__ part,
+                                                   int* __restrict__ sync,
+                                                   int* __restrict__ fault) {
+  constexpr int CH = kRowsKC / 8;                 // 16-byte chunks per row of a slice
+  constexpr int WUNITS = 64 * CH;                 // weight units (16 bytes) per slice
+  constexpr int XUNITS = NT * 16 * TM * CH;       // activation units per slice
+  constexpr int PL = (WUNITS + XUNITS) / 256;     // units per lane per slice
+  constexpr int STAGE = (WUNITS + XUNITS) * 8;    // bf16 elements per stage
+  static_assert((WUNITS + XUNITS) % 256 == 0, "whole instructions per slice");
+  extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+
+  const int T = (N + 63) / 64;
+  const int loc = blockIdx.x / 8;
+  const int t = blockIdx.x % 8 + 8 * (loc / nsplit), split = loc % nsplit;
+  if (t >= T) return;
+  const int n0 = t * 64, kbeg = split * ks;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+
+  // unit u = (i * 4 + wave) * 64 + lane of a stage: weight row u / CH for u <
+  // WUNITS, else activation plane / row; its LDS chunk u % CH holds the row's
+  // global chunk (u % CH) ^ (row & 15)
+  const bf16_t* src[PL];
+#pragma unroll
+  for (int i = 0; i < PL; ++i) {
+    const int u = (i * 4 + wave) * 64 + lane;
+    if (u < WUNITS) {
+      const int r = u / CH, c = (u % CH) ^ (r & 15);
+      src[i] = W + (size_t)min(n0 + r, N - 1) * K + kbeg + c * 8;
+    } else {
+      const int v = u - WUNITS, p = v / (16 * TM * CH), r = (v / CH) % (16 * TM);
+      const int c = (v % CH) ^ (r & 15);
+      src[i] = A + p * a_plane + (size_t)min(r, M - 1) * lda + kbeg + c * 8;
+    }
+  }
+  auto issue = [&](int stage, int kt) {
+    bf16_t* sb = smem + stage * STAGE;
+#pragma unroll
+    for (int i = 0; i < PL; ++i) dma16(src[i] + kt * kRowsKC, sb + (i * 4 + wave) * 512);
+  };
+
+  floatx4_t acc[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) acc[i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  const int fr = lane & 15, g = lane >> 4;
+  const int KT = ks / kRowsKC;
+#pragma unroll
+  for (int s = 0; s < kRowsStages - 1; ++s)
+    if (s < KT) issue(s, s);
+  for (int kt = 0; kt < KT; ++kt) {
+    const int ahead = min(kRowsStages - 2, KT - 1 - kt);  // later slices already issued
+    if (ahead >= 2) wait_vm_lgkm<2 * PL>();
+    else if (ahead == 1) wait_vm_lgkm<PL>();
+    else wait_vm_lgkm<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kt + kRowsStages - 1 < KT) issue((kt + kRowsStages - 1) % kRowsStages, kt + kRowsStages - 1);
+    const bf16_t* sb = smem + (kt % kRowsStages) * STAGE;
+    const bf16_t* xb = sb + WUNITS * 8;
+#pragma unroll
+    for (int st = 0; st < kRowsKC / kBK; ++st) {
+      const int c = 4 * st + g;  // this lane's chunk of the 32-deep step
+      const int wr = wave * 16 + fr;
+      const bf16x8_t wf = *reinterpret_cast<const bf16x8_t*>(sb + (wr * CH + (c ^ (wr & 15))) * 8);
+#pragma unroll
+      for (int p = 0; p < NT; ++p)
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int xr = i * 16 + fr;
+          const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(
+              xb + ((p * 16 * TM + xr) * CH + (c ^ (xr & 15))) * 8);
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf, wf, acc[i], 0, 0, 0);
+        }
+    }
+  }
+
+  if (nsplit > 1) {
+    __shared__ int s_last;
+    floatx4_t* slab = part + ((size_t)(t * nsplit + split) * 4 * TM + wave * TM) * 64;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) slab[i * 64 + lane] = acc[i];
+    const int me = xcc_id();
+    int* line = sync + (size_t)t * kRowsSyncLine;
+    if (tid == 0) line[32 + split] = me;
+    // this thread's stores have reached the L2 (the empty asm keeps the compiler
+    // from moving memory operations across the wait)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("" ::: "memory");
+    __syncthreads();
+    if (tid == 0) {
+      const int old = __hip_atomic_fetch_add(line, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      s_last = old == nsplit - 1;
+      if (old == nsplit - 1)  // reset for the next launch
+        __hip_atomic_exchange(line, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    __syncthreads();
+    if (!s_last) return;
+    // drop this CU's L1 (it may hold lines of the partials from before their
+    // stores); the loads below also bypass it (sc0)
+    asm volatile("buffer_inv sc0" ::: "memory");
+    const __amdgpu_buffer_rsrc_t rp =
+        rsrc(part + (size_t)t * nsplit * 4 * TM * 64, (size_t)nsplit * 4 * TM * 64 * 16);
+    const __amdgpu_buffer_rsrc_t rs = rsrc(line, kRowsSyncLine * 4);
+    if (wave == 0 && lane < nsplit) {
+      const int xo = __builtin_amdgcn_raw_buffer_load_b32(rs, (32 + lane) * 4, 0, 1);
+      if (xo != me) *fault = 1;
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      floatx4_t sum = floatx4_t{0.f, 0.f, 0.f, 0.f};
+      for (int sp = 0; sp < nsplit; ++sp) {
+        const u32x4_t v = load_l2(rp, (int)((((size_t)sp * 4 * TM + wave * TM + i) * 64 + lane) * 16));
+        sum[0] += __uint_as_float(v.x); sum[1] += __uint_as_float(v.y);
+        sum[2] += __uint_as_float(v.z); sum[3] += __uint_as_float(v.w);
+      }
+      acc[i] = sum;
+    }
+  }
+  // epilogue (lane: rows 16 i + 4 g + r, column n0 + 16 wave + fr)
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = i * 16 + 4 * g + r, n = n0 + wave * 16 + fr;
+      const float v = acc[i][r];
+      const float o = EPI == GEMV_SWIGLU ? pair_swap(v) : 0.f;
+      epi_out<EPI>(C, ldc, H, ldh, M, N, m, n, v, o);
+    }
+}
+
 // ------------------------------------------------------------------- vector fp32
 template <typename WT, int EPI>
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, int lda,
@@ -684,6 +844,23 @@ static hipError_t gemm_skinny(const ActBuf& A, int lda, const void* W, int M, in
 #undef WICI_SKT
 }
 
+template <int NT, int TM, int EPI>
+static hipError_t gemm_rows_launch(const ActBuf& A, int lda, const void* W, int M, int N, int K,
+                                   int nsplit, float* C, int ldc, const ActBuf& H, int ldh,
+                                   float* part, int* sync, int* fault, hipStream_t st) {
+  const int T = (N + 63) / 64;
+  const int grid = 8 * ((T + 7) / 8) * nsplit;
+  const size_t lds = (size_t)kRowsStages * (64 + NT * 16 * TM) * kRowsKC * sizeof(bf16_t);
+  auto fn = &k_gemm_rows<NT, TM, EPI>;
+  if (lds > 65536)
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipLaunchKernelGGL(fn, dim3(grid), dim3(256), lds, st, A.planes, A.plane_stride, lda,
+                     static_cast<const bf16_t*>(W), M, N, K, nsplit, K / nsplit, C, ldc, H, ldh,
+                     reinterpret_cast<floatx4_t*>(part), sync, fault);
+  return hipGetLastError();
+}
+
 template <typename WT, int EPI>
 static hipError_t gemm_f32(const ActBuf& A, int lda, const WT* W, int M, int N, int K, float* C,
                            int ldc, const ActBuf& H, int ldh, hipStream_t st) {
@@ -733,6 +910,46 @@ hipError_t launch_gemm_split(int wt, const ActBuf& A, int lda, const void* W, in
     case 3: return gemm_split_nt<3>(wt, A, lda, W, M, N, K, nsplit, P, p_split, st);
     default: return hipErrorInvalidValue;
   }
+}
+
+// Splits along K for the few-rows kernel: the fewest (up to 16) that give at
+// least 384 workgroups with whole 128-deep slices, as far as the partials fit
+// `part_floats` and the tiles the sync lines.
+int gemm_rows_splits(int M, int N, int K, size_t part_floats) {
+  const int T = (N + 63) / 64, TM = M <= 16 ? 1 : 2;
+  if (T > kRowsMaxTiles) return 1;
+  int best = 1;
+  for (int s = 2; s <= 16 && T * best < 384; ++s) {
+    if (K % (s * kRowsKC)) continue;
+    if ((size_t)T * s * 4 * TM * 64 * 4 > part_floats) break;
+    best = s;
+  }
+  return best;
+}
+
+hipError_t launch_gemm_rows(int wt, int epi, const ActBuf& A, int lda, const void* W, int M,
+                            int N, int K, float* C, int ldc, const ActBuf& H, int ldh,
+                            float* part, size_t part_floats, int* sync, int* fault,
+                            hipStream_t st) {
+  if (wt != W_BF16 || A.nt < 1 || A.nt > 3 || M < 1 || M > 32 || K % kRowsKC)
+    return launch_gemm(wt, epi, A, lda, W, M, N, K, C, ldc, H, ldh, st);
+  const int nsplit = part && sync && fault ? gemm_rows_splits(M, N, K, part_floats) : 1;
+#define WICI_RW(NT_, TM_, E) \
+  gemm_rows_launch<NT_, TM_, E>(A, lda, W, M, N, K, nsplit, C, ldc, H, ldh, part, sync, fault, st)
+#define WICI_RW_NT(E)                                                        \
+  switch (A.nt) {                                                            \
+    case 1: return M <= 16 ? WICI_RW(1, 1, E) : WICI_RW(1, 2, E);            \
+    case 2: return M <= 16 ? WICI_RW(2, 1, E) : WICI_RW(2, 2, E);            \
+    default: return M <= 16 ? WICI_RW(3, 1, E) : WICI_RW(3, 2, E);           \
+  }
+  switch (epi) {
+    case GEMV_STORE: WICI_RW_NT(GEMV_STORE)
+    case GEMV_RESID: WICI_RW_NT(GEMV_RESID)
+    case GEMV_SWIGLU: WICI_RW_NT(GEMV_SWIGLU)
+    default: return hipErrorInvalidValue;
+  }
+#undef WICI_RW_NT
+#undef WICI_RW
 }
 
 hipError_t launch_gemm(int wt, int epi, const ActBuf& A, int lda, const void* W, int M, int N,

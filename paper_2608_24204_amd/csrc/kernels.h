@@ -198,6 +198,20 @@ hipError_t launch_gemm(int wt, int epi, const ActBuf& A, int lda, const void* W,
 hipError_t launch_gemm_split(int wt, const ActBuf& A, int lda, const void* W, int M, int N, int K,
                              int nsplit, float* P, size_t p_split, hipStream_t st);
 int gemm_split_count(int wt, int nt, int M, int N, int K, int max_split);
+// The product for at most 32 rows (a batched decode step), bf16 weights, nt >= 1,
+// K a multiple of 128, staged through LDS in whole lines; otherwise, or for other
+// weight types, launch_gemm.  With part (part_floats floats), sync
+// (kGemmRowsSyncInts ints, zero before the first launch and zero again after
+// every launch) and fault all non-null, products with few weight rows are split
+// along K and summed in the launch by the last split of each 64-row tile, all
+// splits of a tile on one XCD; *fault is set to 1 if they were not (the result
+// cannot be trusted then).  Launches that share sync must not overlap.
+constexpr int kGemmRowsSyncInts = 512 * 64;
+int gemm_rows_splits(int M, int N, int K, size_t part_floats);
+hipError_t launch_gemm_rows(int wt, int epi, const ActBuf& A, int lda, const void* W, int M,
+                            int N, int K, float* C, int ldc, const ActBuf& H, int ldh,
+                            float* part, size_t part_floats, int* sync, int* fault,
+                            hipStream_t st);
 // x[t] += sum over s < nsplit of P[s * p_split + t * d] (in that order) for T rows
 // of width d; then, with gain != nullptr, y[t] = RMSNorm(x[t]) * gain (as
 // launch_rmsnorm_rows).

@@ -66,7 +66,7 @@ struct Layout {
   size_t kv_layer_stride, kv_bytes;
   // scratch
   size_t x, a, qkv, att, h, kpart, logits, parts, part_o, part_ml, tokens, table, state, hist,
-      seqs, attn_sync;
+      seqs, attn_sync, gemm_sync;
   size_t scratch_bytes;
   int nsplit;
 };
@@ -172,6 +172,8 @@ Layout make_layout(const wici_config& c) {
   L.seqs = o; o = align_up(o + (size_t)kMaxBatch * sizeof(wici::SeqDesc));  // batched decode
   // counters and XCD records of the decode attention's in-launch merge
   L.attn_sync = o; o = align_up(o + (size_t)wici::attn_fuse_ints(c.n_kv_heads) * 4);
+  // counters and XCD records of the batched products' split-K sums
+  L.gemm_sync = o; o = align_up(o + (size_t)wici::kGemmRowsSyncInts * 4);
   L.scratch_bytes = o;
   return L;
 }
@@ -495,6 +497,17 @@ hipError_t enqueue_decode_batch(wici_model* m, int B) {
   const float q_scale = 1.0f / std::sqrt((float)c.head_dim);
   hipStream_t s = m->stream;
   hipError_t e;
+  // the products: split-K partials in the prefill's split buffer, a misplaced
+  // split reported through the lead sequence's state
+  float* gpart = m->S<float>(L.kpart);
+  const size_t gpart_floats = (size_t)kMaxKSplit * C * d;
+  int* gsync = m->S<int>(L.gemm_sync);
+  int* gfault = &reinterpret_cast<DecodeState*>(m->ds + L.state)->fault;
+  auto prod = [&](int epi, const wici::ActBuf& in, int K, size_t w, int N, float* out, int ldo,
+                  const wici::ActBuf& hout, int ldh) {
+    return wici::launch_gemm_rows(wb, epi, in, K, m->dw + w, B, N, K, out, ldo, hout, ldh,
+                                  gpart, gpart_floats, gsync, gfault, s);
+  };
 #define WICI_TRY(call) \
   do {                 \
     if ((e = (call))) return e; \
@@ -505,24 +518,21 @@ hipError_t enqueue_decode_batch(wici_model* m, int B) {
   for (int l = 0; l < c.n_layers; ++l) {
     WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_anorm)), c.rms_eps, B, d,
                                        a, s));
-    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_STORE, rd(a, pl.qkv), d, m->dw + m->layer(l, L.l_wqkv), B,
-                               nqkv, d, qkv, nqkv, none, 0, s));
+    WICI_TRY(prod(wici::GEMV_STORE, rd(a, pl.qkv), d, m->layer(l, L.l_wqkv), nqkv, qkv, nqkv,
+                  none, 0));
     WICI_TRY(wici::launch_rope_append_batch(kb, qkv, B, c.n_heads, m->W<float>(L.rope_cos),
                                             m->W<float>(L.rope_sin), seqs, l, kv, q_scale, s));
     WICI_TRY(wici::launch_attn_decode_batch(kb, qkv, nqkv, B, c.n_heads, kv, seqs, l, L.nsplit,
                                             part_o, part_ml, att, s));
-    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_RESID, rd(att, pl.o), qd, m->dw + m->layer(l, L.l_wo), B, d,
-                               qd, x, d, none, 0, s));
+    WICI_TRY(prod(wici::GEMV_RESID, rd(att, pl.o), qd, m->layer(l, L.l_wo), d, x, d, none, 0));
     WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_fnorm)), c.rms_eps, B, d,
                                        a, s));
-    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_SWIGLU, rd(a, pl.gu), d, m->dw + m->layer(l, L.l_wgu), B,
-                               2 * F, d, nullptr, 0, h, F, s));
-    WICI_TRY(wici::launch_gemm(wb, wici::GEMV_RESID, rd(h, pl.down), F, m->dw + m->layer(l, L.l_wdown), B, d,
-                               F, x, d, none, 0, s));
+    WICI_TRY(prod(wici::GEMV_SWIGLU, rd(a, pl.gu), d, m->layer(l, L.l_wgu), 2 * F, nullptr, 0, h,
+                  F));
+    WICI_TRY(prod(wici::GEMV_RESID, rd(h, pl.down), F, m->layer(l, L.l_wdown), d, x, d, none, 0));
   }
   WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(L.final_norm), c.rms_eps, B, d, a, s));
-  WICI_TRY(wici::launch_gemm(wb, wici::GEMV_STORE, a, d, m->dw + L.lm_head, B, c.vocab, d, logits,
-                             c.vocab, none, 0, s));
+  WICI_TRY(prod(wici::GEMV_STORE, a, d, L.lm_head, c.vocab, logits, c.vocab, none, 0));
   WICI_TRY(wici::launch_argmax_rows(logits, B, c.vocab, seqs, s));
 #undef WICI_TRY
   return hipSuccess;
@@ -550,14 +560,16 @@ hipError_t alloc_state_mirror(wici_model* m) {
   return hipHostGetDevicePointer((void**)&m->d_state_mirror, m->h_state, 0);
 }
 
-// The decode attention's in-launch merge found the split blocks of a KV head
-// on different XCDs, so partials may have been read before they were visible:
-// the results of the step cannot be trusted and the model stops here.
+// An in-launch merge (the decode attention's, or a batched product's split-K
+// sum) found its split blocks on different XCDs, so partials may have been read
+// before they were visible: the results of the step cannot be trusted and the
+// model stops here.
 wici_status placement_fault(wici_model* m) {
   m->failed = true;
   m->have_token = false;
-  return fail(m, WICI_E_HIP, "decode attention: the split blocks of a KV head did not all run "
-                             "on one XCD (workgroups not dealt to the XCDs in turn)");
+  return fail(m, WICI_E_HIP, "decode step: the split blocks of an attention head or of a "
+                             "product tile did not all run on one XCD (workgroups not dealt to "
+                             "the XCDs in turn)");
 }
 
 // Clear the mirror's `done` before queueing work whose final argmax writes it.
@@ -696,6 +708,8 @@ wici_status wici_bind_memory(wici_model* m, void* d_weights, size_t weight_bytes
   HIP_TRY(m, wici::launch_reset_state(m->ds + m->L.state, m->stream));
   HIP_TRY(m, wici::launch_fill_i32(m->S<int32_t>(m->L.attn_sync),
                                    wici::attn_fuse_ints(m->cfg.n_kv_heads), 0, m->stream));
+  HIP_TRY(m, wici::launch_fill_i32(m->S<int32_t>(m->L.gemm_sync), wici::kGemmRowsSyncInts, 0,
+                                   m->stream));
   HIP_TRY(m, hipStreamSynchronize(m->stream));
   m->bound = true;
   m->pos = 0;
@@ -984,6 +998,8 @@ wici_status wici_bind_memory_shared(wici_model* m, const wici_model* src, void* 
   HIP_TRY(m, wici::launch_reset_state(m->ds + m->L.state, m->stream));
   HIP_TRY(m, wici::launch_fill_i32(m->S<int32_t>(m->L.attn_sync),
                                    wici::attn_fuse_ints(m->cfg.n_kv_heads), 0, m->stream));
+  HIP_TRY(m, wici::launch_fill_i32(m->S<int32_t>(m->L.gemm_sync), wici::kGemmRowsSyncInts, 0,
+                                   m->stream));
   HIP_TRY(m, hipStreamSynchronize(m->stream));
   m->loaded.assign(m->specs.size(), 1);
   m->n_loaded = (int)m->specs.size();
@@ -1069,6 +1085,7 @@ wici_status wici_decode_batch(wici_model* const* models, int32_t n, const int32_
     HIP_TRY(lead, hipMemcpyAsync(logits, lead->ds + L.h, (size_t)n * c.vocab * 4,
                                  hipMemcpyDeviceToHost, lead->stream));
   HIP_TRY(lead, hipStreamSynchronize(lead->stream));
+  if (st[0].fault) return placement_fault(lead);
   int bad = -1;
   for (int b = 0; b < n; ++b) {
     models[b]->pos = st[b].pos;

@@ -72,6 +72,38 @@ def test_batched_decode_matches_oracle_per_sequence(cuda_ok, kind, cap):
         assert rep.strict_ids, rep.summary()
 
 
+@pytest.mark.parametrize("n", [20, 33])
+def test_large_batches_match_oracle(cuda_ok, n):
+    """17-32 sequences: the batched products take the rows in two 16-row tiles
+    (split along K for the projections with few weight rows, summed in the
+    launch); past 32 they are the prefill's matrix-core products."""
+    cfg = CFGS["bf16"]
+    w = inputs.make_weights(cfg, gain_std=0.1)
+    w64 = inputs.weights_f64(cfg, w)
+    steps = 5
+    rng = np.random.default_rng(11)
+    ps = [rng.integers(0, cfg.vocab, 20 + 3 * b).astype(np.int32) for b in range(n)]
+    ms = clients(cfg, w, n, kv_page=16, max_seq=140)
+    try:
+        ids = [[m.prefill(p)[0]] for m, p in zip(ms, ps)]
+        logs = [[] for _ in range(n)]
+        for _ in range(steps):
+            toks, lg = ms[0].decode_batch(ms, want_logits=True)
+            for b in range(n):
+                ids[b].append(int(toks[b]))
+                logs[b].append(lg[b])
+    finally:
+        for m in ms:
+            m.close()
+    for b in range(n):
+        ora_ids, ora = oracle_run(cfg, w64, ps[b], steps)
+        # the prefill's logits are not compared here: only the batched steps
+        rep = compare(ids[b], [None] + logs[b], ora_ids, ora)
+        print(f"[batch] n={n} seq {b} (P={len(ps[b])}): {rep.summary()}", flush=True)
+        assert rep.max_rel_err <= 2e-2
+        assert rep.strict_ids, rep.summary()
+
+
 def test_shared_weights_and_batch_agree_with_single_decoding(cuda_ok):
     from paper_2608_24204_amd.binding import WiciModel
     cfg = CFGS["bf16"]

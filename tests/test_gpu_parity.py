@@ -86,8 +86,13 @@ def test_tiny_config(cuda_ok):
 
 
 @pytest.mark.parametrize("P,chunk,page", [(1, 64, 16), (63, 64, 16), (65, 64, 32),
-                                          (200, 64, 16), (129, 128, 128), (300, 2048, 64)])
+                                          (200, 64, 16), (129, 128, 128), (300, 2048, 64),
+                                          (700, 2048, 64), (1000, 384, 16)])
 def test_ragged_prompts_chunks_and_pages(cuda_ok, P, chunk, page):
+    """From 8 key blocks of 64 the prefill attention splits the longest key walks
+    in two and merges them: 700 positions in one chunk split query blocks 6..10
+    (the last one ragged) and leave 0..5 whole; 1000 in chunks of 384 split
+    every query block of the later chunks."""
     cfg = SMALL["gqa128_bf16"]
     prompt = inputs.make_prompt(cfg, P)
     rep, _, _ = run_parity(cfg, prompt, 20, gain_std=0.1, prefill_chunk=chunk, kv_page=page,
