@@ -272,6 +272,29 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
     if (n > 0) attn_merge_in_last_split<HD, G>(fz, g, split, nsplit, n, part_o, part_ml);
 }
 
+// Long contexts (more 64-position splits than the merge in the last split block
+// takes): the same launch with each block walking `span` consecutive sub-chunks
+// (attn_span_mfma, four teams of four wavefronts), so that the splits of a head
+// are at most kFuseMaxSplits, and the merge in the last of them.  Block
+// placement as k_attn_decode_mfma's FUSE.
+constexpr int kSpanTeams = 4;  // workgroups of 4 x 4 wavefronts
+template <int HD, int G>
+__global__ __launch_bounds__(256 * kSpanTeams) void k_attn_decode_span(const float* __restrict__ q_in,
+                                                          KvLayout kv,
+                                                          const DecodeState* __restrict__ st,
+                                                          float* __restrict__ part_o,
+                                                          float* __restrict__ part_ml,
+                                                          AttnFuse fz, int span) {
+  static_assert(G <= 16 && G * HD <= 512, "as the merge in the last split block");
+  const int Hkv = kv.n_kv;
+  const int b = blockIdx.x, x = b & 7, r = b >> 3, h8 = (Hkv + 7) >> 3;
+  const int g = x + 8 * (r % h8), split = r / h8, nsplit = fz.nsplit;
+  if (g >= Hkv) return;
+  const int n =
+      attn_span_mfma<HD, G, kSpanTeams>(q_in, kv, st, part_o, part_ml, g, split, nsplit, span);
+  if (n > 0) attn_merge_in_last_split<HD, G>(fz, g, split, nsplit, n, part_o, part_ml, span);
+}
+
 // out[h, d] = sum_s e^(m_s - M) o_s[d] / sum_s e^(m_s - M) l_s over the active
 // splits s of head h, for launches of at most kMergePf splits (grid Hq, HD
 // threads).  The position, the first 64 splits' statistics and the thread's
@@ -440,6 +463,21 @@ static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const Decod
       const int blocks = 8 * ((kv.n_kv + 7) / 8) * nsplit;
       launch_k(k_attn_decode_mfma<HD, G, true>, dim3(blocks), dim3(256), 0, s, kOnly, q, kv, st,
                part_o, part_ml, (const SeqDesc*)nullptr, 0, 0, fz);
+      return hipGetLastError();
+    }
+    // longer: splits of several sub-chunks, as few as keep them within the merge
+    // (8.2K positions: 26 splits of 5 sub-chunks instead of 130 splits and a
+    // merge kernel)
+    const int span = (nsplit + kFuseMaxSplits - 1) / kFuseMaxSplits;
+    if (fuse && span <= kMaxSpan) {
+      AttnFuse fz = *fuse;
+      fz.out = out;
+      fz.nsplit = (nsplit + span - 1) / span;
+      fz.n_heads = Hq;
+      fz.n_kv = kv.n_kv;
+      const int blocks = 8 * ((kv.n_kv + 7) / 8) * fz.nsplit;
+      launch_k(k_attn_decode_span<HD, G>, dim3(blocks), dim3(256 * kSpanTeams), 0, s, kOnly, q,
+               kv, st, part_o, part_ml, fz, span);
       return hipGetLastError();
     }
   }

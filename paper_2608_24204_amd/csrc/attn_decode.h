@@ -33,7 +33,7 @@ template <int HD, int G>
 __device__ __forceinline__ void attn_merge_in_last_split(const AttnFuse& fz, int g, int split,
                                                          int nsplit, int n,
                                                          const float* part_o,
-                                                         const float* part_ml) {
+                                                         const float* part_ml, int span = 1) {
   constexpr int COLS = G * HD / 4;      // float4 columns of the group's output
   constexpr int P = 256 / COLS;         // threads per column (>= 2)
   constexpr int PER = kFuseMaxSplits / P;
@@ -41,7 +41,7 @@ __device__ __forceinline__ void attn_merge_in_last_split(const AttnFuse& fz, int
   __shared__ float s_w[G][kFuseMaxSplits];
   __shared__ float4 s_red[P][COLS];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int active = (n + kChunk - 1) / kChunk;
+  const int active = (n + kChunk * span - 1) / (kChunk * span);  // splits holding positions
   const int me = xcc_id();
   if (tid == 0) fz.xcc[g * kFuseLine + split] = me;
   // this thread's stores have reached the L2 (the empty asm keeps the compiler
@@ -81,7 +81,7 @@ __device__ __forceinline__ void attn_merge_in_last_split(const AttnFuse& fz, int
     }
   }
   // statistics: one wavefront per head, lane = split
-  for (int h = wave; h < G; h += 4) {
+  for (int h = wave; h < G; h += (int)(blockDim.x >> 6)) {
     const int hq = g * G + h, sp = min(lane, active - 1);
     const size_t f = ((size_t)hq * nsplit + sp) * 2;   // float index of (m, l)
     const u32x4_t st2 = load_l2(rm, (int)((f & ~(size_t)3) * 4));
@@ -280,6 +280,225 @@ __device__ __forceinline__ int attn_split_mfma(const float* __restrict__ q_in, c
     float acc = 0.f, L = 0.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
+      const float e = wm[w][h] == -INFINITY ? 0.f : __expf(wm[w][h] - M);
+      acc += e * wo[w][h][d];
+      L += e * wl[w][h];
+    }
+    const int hh = g * G + h;
+    part_o[((size_t)hh * nsplit + split) * HD + d] = acc;
+    if (d == 0) {
+      part_ml[((size_t)hh * nsplit + split) * 2 + 0] = M;
+      part_ml[((size_t)hh * nsplit + split) * 2 + 1] = L;
+    }
+  }
+  return n;
+}
+
+// A split of `span` consecutive 64-position sub-chunks (long contexts, so that
+// the splits of a head stay few enough for the merge in the last split block):
+// positions [64 span split, 64 span (split + 1)) of KV head g, all G query
+// heads, by a workgroup of TEAMS x 4 wavefronts.  Team t takes sub-chunks t,
+// t + TEAMS, ..., each multiplied as in attn_split_mfma (wavefront w of the
+// team: positions 16 w .. 16 w + 15 of it); a wavefront carries its (max, sum)
+// and output rows across its sub-chunks (online softmax: the running values
+// are rescaled by e^(m_old - m_new) when the max grows), and all 4 TEAMS
+// wavefronts are combined at the end.  The teams' wavefronts hide each other's
+// load and matrix-chain latencies (one team of four walking every sub-chunk
+// leaves under one wavefront per SIMD on the chip: 8.2K positions 18.5 us per
+// layer, two teams with two sub-chunks in flight each 14.1 us).  The query's
+// bf16 terms sit in LDS (the same fragments in every wavefront) to keep the
+// registers within four wavefronts per SIMD.  The split's page-table entries
+// are requested with the query.  Writes and returns as attn_split_mfma.
+constexpr int kMaxSpan = 8;
+template <int HD, int G, int TEAMS>
+__device__ __forceinline__ int attn_span_mfma(const float* __restrict__ q_in, const KvLayout& kv,
+                                              const DecodeState* __restrict__ st,
+                                              float* __restrict__ part_o,
+                                              float* __restrict__ part_ml, int g, int split,
+                                              int nsplit, int span) {
+  constexpr int DS = HD / 32;  // 32-deep steps of S^T
+  constexpr int DT = HD / 16;  // 16-wide output tiles of P V
+  constexpr int VP = 16 + 4;   // LDS row of one dimension's 16 positions
+  constexpr int NW = 4 * TEAMS;
+  __shared__ bf16_t vt[NW][HD][VP];
+  __shared__ float wm[NW][G], wl[NW][G];
+  __shared__ float wo[NW][G][HD];
+
+  const int Hkv = kv.n_kv;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int team = wave >> 2, wq = wave & 3;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int start = split * kChunk * span;
+  const int ps = __ffs(kv.page) - 1;
+  const bf16_t* base = static_cast<const bf16_t*>(kv.base);
+  const size_t head_stride = (size_t)kv.page * HD;
+
+  // this lane's position in each of its team's sub-chunks and the page, the
+  // query and the context length, requested together
+  constexpr int MJ = (kMaxSpan + TEAMS - 1) / TEAMS;  // sub-chunks per team at most
+  int phys[MJ];
+#pragma unroll
+  for (int j = 0; j < MJ; ++j) {
+    const int c = team + TEAMS * j;
+    const int jc = min(start + c * kChunk + 16 * wq + r16, kv.max_pos - 1);
+    phys[j] = c < span ? kv.table[jc >> ps] : 0;
+  }
+  float qv[DS][8];
+  {
+    const float* qr = q_in + ((size_t)g * G + min(r16, G - 1)) * HD + 8 * g4;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      const float4 a = *reinterpret_cast<const float4*>(qr + 32 * s);
+      const float4 b = *reinterpret_cast<const float4*>(qr + 32 * s + 4);
+      qv[s][0] = a.x; qv[s][1] = a.y; qv[s][2] = a.z; qv[s][3] = a.w;
+      qv[s][4] = b.x; qv[s][5] = b.y; qv[s][6] = b.z; qv[s][7] = b.w;
+    }
+  }
+  const int n = st->pos + 1;
+  if (start >= n) return 0;
+  const int nsub = min(span, (n - start + kChunk - 1) / kChunk);
+  const int nj = nsub > team ? (nsub - team + TEAMS - 1) / TEAMS : 0;  // this team's sub-chunks
+
+  bf16x8_t kf[1][DS];  // one sub-chunk per wavefront at a time
+  uint4 vr[1][DS];
+  auto load = [&](int b, int j) {
+    const int c = team + TEAMS * j;
+    const int jc = min(start + c * kChunk + 16 * wq + r16, kv.max_pos - 1);
+    int pp = phys[0];
+#pragma unroll
+    for (int i = 1; i < MJ; ++i) pp = j == i ? phys[i] : pp;
+    const bf16_t* pk = base + (((size_t)pp * 2 + 0) * Hkv + g) * head_stride +
+                       (size_t)(jc & (kv.page - 1)) * HD + 8 * g4;
+    const bf16_t* pv = pk + (size_t)Hkv * head_stride;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      kf[b][s] = *reinterpret_cast<const bf16x8_t*>(pk + 32 * s);
+      vr[b][s] = *reinterpret_cast<const uint4*>(pv + 32 * s);
+    }
+  };
+  // the query as three bf16 terms (columns past G are zero), in LDS: every
+  // wavefront reads the same fragments, which would hold 48 registers
+  __shared__ bf16x8_t qlds[3][DS][64];
+  if (wave == 0) {
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      bf16x8_t qt[3];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float v = r16 < G ? qv[s][e] : 0.f;
+#pragma unroll
+        for (int t = 0; t < 3; ++t) {
+          const __bf16 b = static_cast<__bf16>(v);
+          qt[t][e] = b;
+          v -= static_cast<float>(b);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 3; ++t) qlds[t][s][lane] = qt[t];
+    }
+  }
+  __syncthreads();
+  if (nj > 0) load(0, 0);
+
+  float m_run = -INFINITY, l_run = 0.f;  // of head r16 over this wavefront's positions
+  floatx4_t o[DT];                       // lane: O[head 4 g4 + i][dimension 16 u + r16]
+#pragma unroll
+  for (int u = 0; u < DT; ++u) o[u] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  auto process = [&](int b, int j) {
+    const int c0 = start + (team + TEAMS * j) * kChunk + 16 * wq;  // first position
+    // values transposed into this wavefront's LDS tile (zero past the context);
+    // the tile is the wavefront's own, and the previous sub-chunk's reads of it
+    // have returned (their matrix ops consumed them) before these stores
+    const bool valid = c0 + r16 < n;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      const unsigned w4[4] = {vr[b][s].x, vr[b][s].y, vr[b][s].z, vr[b][s].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const unsigned w = valid ? w4[e] : 0u;
+        vt[wave][32 * s + 8 * g4 + 2 * e][r16] = (bf16_t)(w & 0xffffu);
+        vt[wave][32 * s + 8 * g4 + 2 * e + 1][r16] = (bf16_t)(w >> 16);
+      }
+    }
+    // the tile's stores are done before any lane reads it (lgkmcnt 0 alone)
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_wave_barrier();
+    floatx4_t sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < DS; ++s)
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[b][s], qlds[t][s][lane], sc, 0, 0, 0);
+    float mc = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (c0 + 4 * g4 + i >= n) sc[i] = -INFINITY;
+      mc = fmaxf(mc, sc[i]);
+    }
+    mc = fmaxf(mc, __shfl_xor(mc, 16));
+    mc = fmaxf(mc, __shfl_xor(mc, 32));
+    const float m_new = fmaxf(m_run, mc);
+    const float corr = m_new == -INFINITY ? 1.f : __expf(m_run - m_new);
+    float p[4], lc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p[i] = sc[i] == -INFINITY ? 0.f : __expf(sc[i] - m_new);
+      lc += p[i];
+    }
+    lc += __shfl_xor(lc, 16);
+    lc += __shfl_xor(lc, 32);
+    l_run = l_run * corr + lc;
+    m_run = m_new;
+    short4_t pa[3];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = p[i];
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+        const __bf16 bb = static_cast<__bf16>(v);
+        pa[t][i] = __builtin_bit_cast(short, bb);
+        v -= static_cast<float>(bb);
+      }
+    }
+    // rescale the output rows (heads 4 g4 + i) by their heads' factors
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float cr = __shfl(corr, 4 * g4 + i);
+#pragma unroll
+      for (int u = 0; u < DT; ++u) o[u][i] *= cr;
+    }
+#pragma unroll
+    for (int u = 0; u < DT; ++u) {
+      const short4_t vb = *reinterpret_cast<const short4_t*>(&vt[wave][16 * u + r16][4 * g4]);
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+        o[u] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vb, o[u], 0, 0, 0);
+    }
+  };
+  for (int j = 0; j < nj; ++j) {
+    if (j > 0) load(0, j);
+    process(0, j);
+  }
+
+  // combine the wavefronts (one without positions has max -inf and weight 0)
+  if (g4 == 0 && r16 < G) { wm[wave][r16] = m_run; wl[wave][r16] = l_run; }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int h = 4 * g4 + i;
+    if (h < G) {
+#pragma unroll
+      for (int u = 0; u < DT; ++u) wo[wave][h][16 * u + r16] = o[u][i];
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < G * HD; idx += 64 * NW) {
+    const int h = idx / HD, d = idx % HD;
+    float M = wm[0][h];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, wm[w][h]);
+    float acc = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
       const float e = wm[w][h] == -INFINITY ? 0.f : __expf(wm[w][h] - M);
       acc += e * wo[w][h][d];
       L += e * wl[w][h];

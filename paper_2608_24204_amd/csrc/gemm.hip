@@ -523,8 +523,8 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const bf16_t* __restrict__ 
 // bytes) fetched by global_load_lds_dwordx4 in whole 128-byte lines, sixteen
 // lanes to a row.  (Fragment-shaped loads straight into registers touch sixteen
 // rows per instruction, 64 bytes each, and stream no faster than ~4.9 TB/s.)
-// The sixteen 16-byte chunks of a row are XOR-swizzled by the row's low four
-// bits, so a fragment read (sixteen rows, one chunk) covers all 64 banks once.
+// The 16-byte chunks of a row are XOR-swizzled by the row's low bits, so a
+// fragment read (sixteen rows, one chunk) covers all 64 banks once.
 //
 // Products with few weight rows are split along K over grid slots: the splits
 // of a 64-row tile occupy workgroup indices of one residue mod 8, so they run on
@@ -566,31 +566,38 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const bf16_t* __restrict__ A,
 
   // unit u = (i * 4 + wave) * 64 + lane of a stage: weight row u / CH for u <
   // WUNITS, else activation plane / row; its LDS chunk u % CH holds the row's
-  // global chunk (u % CH) ^ (row & 15)
+  // global chunk (u % CH) ^ (row & (CH - 1))
   const bf16_t* src[PL];
 #pragma unroll
   for (int i = 0; i < PL; ++i) {
     const int u = (i * 4 + wave) * 64 + lane;
     if (u < WUNITS) {
-      const int r = u / CH, c = (u % CH) ^ (r & 15);
+      const int r = u / CH, c = (u % CH) ^ (r & (CH - 1));
       src[i] = W + (size_t)min(n0 + r, N - 1) * K + kbeg + c * 8;
     } else {
       const int v = u - WUNITS, p = v / (16 * TM * CH), r = (v / CH) % (16 * TM);
-      const int c = (v % CH) ^ (r & 15);
+      const int c = (v % CH) ^ (r & (CH - 1));
       src[i] = A + p * a_plane + (size_t)min(r, M - 1) * lda + kbeg + c * 8;
     }
   }
+  // Each workgroup starts its walk at its own slice and wraps around: in lockstep
+  // every workgroup would read the same K offset of rows 8 KB apart, which
+  // crowds a few HBM channels.  Offsets of 7 slices between the workgroups of
+  // an XCD and 4 between XCDs measured best (a bare stream of the 8B gate/up
+  // weights: 5.2 -> 6.0 TB/s; offsets of 1 slice: 4.2).
+  const int KT = ks / kRowsKC;
+  const int rot = ((blockIdx.x / 8) * 7 + (blockIdx.x % 8) * 4) % KT;
   auto issue = [&](int stage, int kt) {
     bf16_t* sb = smem + stage * STAGE;
+    const int kk = kt + rot < KT ? kt + rot : kt + rot - KT;
 #pragma unroll
-    for (int i = 0; i < PL; ++i) dma16(src[i] + kt * kRowsKC, sb + (i * 4 + wave) * 512);
+    for (int i = 0; i < PL; ++i) dma16(src[i] + kk * kRowsKC, sb + (i * 4 + wave) * 512);
   };
 
   floatx4_t acc[TM];
 #pragma unroll
   for (int i = 0; i < TM; ++i) acc[i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   const int fr = lane & 15, g = lane >> 4;
-  const int KT = ks / kRowsKC;
 #pragma unroll
   for (int s = 0; s < kRowsStages - 1; ++s)
     if (s < KT) issue(s, s);
@@ -607,14 +614,14 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const bf16_t* __restrict__ A,
     for (int st = 0; st < kRowsKC / kBK; ++st) {
       const int c = 4 * st + g;  // this lane's chunk of the 32-deep step
       const int wr = wave * 16 + fr;
-      const bf16x8_t wf = *reinterpret_cast<const bf16x8_t*>(sb + (wr * CH + (c ^ (wr & 15))) * 8);
+      const bf16x8_t wf = *reinterpret_cast<const bf16x8_t*>(sb + (wr * CH + (c ^ (wr & (CH - 1)))) * 8);
 #pragma unroll
       for (int p = 0; p < NT; ++p)
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
           const int xr = i * 16 + fr;
           const bf16x8_t xf = *reinterpret_cast<const bf16x8_t*>(
-              xb + ((p * 16 * TM + xr) * CH + (c ^ (xr & 15))) * 8);
+              xb + ((p * 16 * TM + xr) * CH + (c ^ (xr & (CH - 1)))) * 8);
           acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf, wf, acc[i], 0, 0, 0);
         }
     }
@@ -852,7 +859,7 @@ static hipError_t gemm_rows_launch(const ActBuf& A, int lda, const void* W, int 
   const int grid = 8 * ((T + 7) / 8) * nsplit;
   const size_t lds = (size_t)kRowsStages * (64 + NT * 16 * TM) * kRowsKC * sizeof(bf16_t);
   auto fn = &k_gemm_rows<NT, TM, EPI>;
-  if (lds > 65536)
+  if (lds >= 65536)
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   hipLaunchKernelGGL(fn, dim3(grid), dim3(256), lds, st, A.planes, A.plane_stride, lda,
@@ -913,13 +920,16 @@ hipError_t launch_gemm_split(int wt, const ActBuf& A, int lda, const void* W, in
 }
 
 // Splits along K for the few-rows kernel: the fewest (up to 16) that give at
-// least 384 workgroups with whole 128-deep slices, as far as the partials fit
-// `part_floats` and the tiles the sync lines.
+// least 192 workgroups with whole 128-deep slices, as far as the partials fit
+// `part_floats` and the tiles the sync lines.  (Measured at 16 rows on the 8B
+// shapes: QKV 2 splits 13.7 us, 4 17.3; O 4 splits 10.6 us, 8 12.1; down 4
+// splits 25.5 us, 7 28.6: more, shorter workgroups pay more in pipeline fill
+// and in the sum.)
 int gemm_rows_splits(int M, int N, int K, size_t part_floats) {
   const int T = (N + 63) / 64, TM = M <= 16 ? 1 : 2;
   if (T > kRowsMaxTiles) return 1;
   int best = 1;
-  for (int s = 2; s <= 16 && T * best < 384; ++s) {
+  for (int s = 2; s <= 16 && T * best < 192; ++s) {
     if (K % (s * kRowsKC)) continue;
     if ((size_t)T * s * 4 * TM * 64 * 4 > part_floats) break;
     best = s;
