@@ -591,7 +591,12 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
   constexpr int BQ = 64, BKEY = 64, DPT = HD / 4;
   __shared__ float Ks[BKEY][HD + 4];
   __shared__ float Vs[BKEY][HD + 4];
-  const int qb = blockIdx.x * BQ, h = blockIdx.y;
+  // the second half of the heads takes the query blocks in reverse order: the
+  // grid is dealt out in order, workgroups b and b + (grid / 2) share a CU when
+  // two fit, and the causal walk of block i is i + 1 key blocks, so this pairs
+  // long walks with short ones on every CU
+  const int qbi = blockIdx.y >= (gridDim.y + 1) / 2 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+  const int qb = qbi * BQ, h = blockIdx.y;
   const int Hkv = kv.n_kv, g = h / (Hq / Hkv);
   const int tid = threadIdx.x, ql = tid >> 2, part = tid & 3;
   const int t = qb + ql;
@@ -680,7 +685,12 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   __shared__ __attribute__((aligned(16))) bf16_t Ks[BKEY][KP];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[HD][VP];
 
-  const int qb = blockIdx.x * BQ, h = blockIdx.y;
+  // the second half of the heads takes the query blocks in reverse order: the
+  // grid is dealt out in order, workgroups b and b + (grid / 2) share a CU when
+  // two fit, and the causal walk of block i is i + 1 key blocks, so this pairs
+  // long walks with short ones on every CU
+  const int qbi = blockIdx.y >= (gridDim.y + 1) / 2 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+  const int qb = qbi * BQ, h = blockIdx.y;
   const int Hkv = kv.n_kv, g = h / (Hq / Hkv);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int l16 = lane & 15, lg = lane >> 4;
