@@ -229,7 +229,10 @@ wici_status wici_bind_memory_shared(wici_model* m, const wici_model* src, void* 
  * n beyond the scratch), WICI_E_STATE (a model not ready, not prefilled or
  * without a token to feed), WICI_E_CAPACITY (a model at max_seq),
  * WICI_E_NUMERIC (a sequence's logits were not finite: its next token is -1,
- * the other sequences advanced normally).  Errors are reported on models[0]. */
+ * the other sequences advanced normally), WICI_E_HIP (a HIP error, or the
+ * workgroups of a product split along K, which add their partial sums through
+ * one XCD's L2 cache, did not all run on the same XCD: the step's results are
+ * then not trusted and models[0] is failed).  Errors are reported on models[0]. */
 wici_status wici_decode_batch(wici_model* const* models, int32_t n, const int32_t* tokens_in,
                               int32_t* next_tokens, float* logits);
 
