@@ -73,7 +73,13 @@ typedef enum {
                               leaves the workloads' greedy ids unchanged, measured) */
 } wici_prefill_mode;
 
-enum { WICI_FLAG_NO_GRAPH = 1 }; /* run decode steps eagerly instead of replaying a graph */
+enum {
+  WICI_FLAG_NO_GRAPH = 1,   /* run decode steps eagerly instead of replaying a graph */
+  WICI_FLAG_FAULT_DRILL = 2 /* for tests of the error path: every in-launch merge (the decode
+                               attention's, the batched products' split-K sums) reports its
+                               splits as run on different XCDs, so decode steps fail with
+                               WICI_E_HIP as they would on a real misplacement */
+};
 
 typedef struct {
   int32_t n_layers;

@@ -24,6 +24,7 @@ STATUS_NAMES = {0: "WICI_OK", -1: "WICI_E_ARG", -2: "WICI_E_STATE", -3: "WICI_E_
 WICI_F32, WICI_BF16, WICI_Q8 = 0, 1, 2
 PREFILL_MODES = {"bf16x2": 0, "bf16": 1, "f32": 2, "bf16x3": 3, "bf16x3q": 4}
 WICI_FLAG_NO_GRAPH = 1
+WICI_FLAG_FAULT_DRILL = 2
 
 # every entry point include/wici.h declares
 EXPORTED = ["wici_create", "wici_memory_requirements", "wici_bind_memory", "wici_load_weights",
@@ -110,7 +111,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
 
 def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool = True,
                 max_seq: int | None = None, prefill_chunk: int | None = None,
-                kv_page: int | None = None, prefill_planes=None) -> WiciConfig:
+                kv_page: int | None = None, prefill_planes=None,
+                fault_drill: bool = False) -> WiciConfig:
     """prefill_planes: None/0 for prefill_mode's own term count, or a tuple
     (qkv, o, gate_up, down[, attention]) of bf16 terms each projection reads and
     the prefill attention carries (bf16x3 only; attention defaults to three)."""
@@ -127,7 +129,7 @@ def make_config(cfg: ModelConfig, prefill_mode: str | None = None, graph: bool =
     c.prefill_chunk = cfg.prefill_chunk if prefill_chunk is None else prefill_chunk
     c.kv_page = cfg.kv_page if kv_page is None else kv_page
     c.prefill_mode = PREFILL_MODES[prefill_mode]
-    c.flags = 0 if graph else WICI_FLAG_NO_GRAPH
+    c.flags = (0 if graph else WICI_FLAG_NO_GRAPH) | (WICI_FLAG_FAULT_DRILL if fault_drill else 0)
     if prefill_planes:
         q, o, gu, dn, *at = prefill_planes
         c.prefill_planes = q | (o << 2) | (gu << 4) | (dn << 6) | ((at[0] if at else 0) << 8)
@@ -241,10 +243,12 @@ class WiciModel:
     def __init__(self, cfg: ModelConfig, *, prefill_mode: str | None = None, graph: bool = True,
                  max_seq: int | None = None, prefill_chunk: int | None = None,
                  kv_page: int | None = None, device: int = 0,
-                 share_weights_of: "WiciModel | None" = None, prefill_planes=None):
+                 share_weights_of: "WiciModel | None" = None, prefill_planes=None,
+                 fault_drill: bool = False):
         """share_weights_of: another (loaded) model whose weights this one uses
         (wici_bind_memory_shared); only the KV cache and scratch are allocated.
-        prefill_planes: see make_config."""
+        prefill_planes: see make_config.  fault_drill: WICI_FLAG_FAULT_DRILL
+        (tests of the misplaced-split error path)."""
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("WiciModel needs a HIP GPU")
@@ -252,7 +256,7 @@ class WiciModel:
         self.lib = load_library()
         self.device = torch.device("cuda", device)
         self.c = make_config(cfg, prefill_mode, graph, max_seq, prefill_chunk, kv_page,
-                             prefill_planes)
+                             prefill_planes, fault_drill)
         wb, kb, sb = memory_requirements(self.c)
         self.mem_bytes = (wb, kb, sb)
         self.stream = torch.cuda.Stream(self.device)

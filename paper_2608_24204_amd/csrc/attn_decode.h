@@ -97,7 +97,7 @@ __device__ __forceinline__ void attn_merge_in_last_split(const AttnFuse& fz, int
     const float e = on ? __expf(mv - M) : 0.f;
     const float L = wave_sum(e * (on ? lv : 0.f));
     if (on) s_w[h][lane] = e / L;
-    if (on && xo != me) static_cast<DecodeState*>(fz.state)->fault = 1;
+    if (on && (xo != me || fz.drill)) static_cast<DecodeState*>(fz.state)->fault = 1;
   }
   __syncthreads();
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);

@@ -548,7 +548,7 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const bf16_t* __restrict__ A,
                                                    float* __restrict__ C, int ldc, ActBuf H,
                                                    int ldh, floatx4_t* __restrict__ part,
                                                    int* __restrict__ sync,
-                                                   int* __restrict__ fault) {
+                                                   int* __restrict__ fault, int drill) {
   constexpr int CH = kRowsKC / 8;                 // 16-byte chunks per row of a slice
   constexpr int WUNITS = 64 * CH;                 // weight units (16 bytes) per slice
   constexpr int XUNITS = NT * 16 * TM * CH;       // activation units per slice
@@ -657,7 +657,7 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const bf16_t* __restrict__ A,
     const __amdgpu_buffer_rsrc_t rs = rsrc(line, kRowsSyncLine * 4);
     if (wave == 0 && lane < nsplit) {
       const int xo = __builtin_amdgcn_raw_buffer_load_b32(rs, (32 + lane) * 4, 0, 1);
-      if (xo != me) *fault = 1;
+      if (xo != me || drill) *fault = 1;
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -854,7 +854,8 @@ static hipError_t gemm_skinny(const ActBuf& A, int lda, const void* W, int M, in
 template <int NT, int TM, int EPI>
 static hipError_t gemm_rows_launch(const ActBuf& A, int lda, const void* W, int M, int N, int K,
                                    int nsplit, float* C, int ldc, const ActBuf& H, int ldh,
-                                   float* part, int* sync, int* fault, hipStream_t st) {
+                                   float* part, int* sync, int* fault, hipStream_t st,
+                                   int drill = 0) {
   const int T = (N + 63) / 64;
   const int grid = 8 * ((T + 7) / 8) * nsplit;
   const size_t lds = (size_t)kRowsStages * (64 + NT * 16 * TM) * kRowsKC * sizeof(bf16_t);
@@ -864,7 +865,7 @@ static hipError_t gemm_rows_launch(const ActBuf& A, int lda, const void* W, int 
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   hipLaunchKernelGGL(fn, dim3(grid), dim3(256), lds, st, A.planes, A.plane_stride, lda,
                      static_cast<const bf16_t*>(W), M, N, K, nsplit, K / nsplit, C, ldc, H, ldh,
-                     reinterpret_cast<floatx4_t*>(part), sync, fault);
+                     reinterpret_cast<floatx4_t*>(part), sync, fault, drill);
   return hipGetLastError();
 }
 
@@ -940,12 +941,13 @@ int gemm_rows_splits(int M, int N, int K, size_t part_floats) {
 hipError_t launch_gemm_rows(int wt, int epi, const ActBuf& A, int lda, const void* W, int M,
                             int N, int K, float* C, int ldc, const ActBuf& H, int ldh,
                             float* part, size_t part_floats, int* sync, int* fault,
-                            hipStream_t st) {
+                            hipStream_t st, bool drill) {
   if (wt != W_BF16 || A.nt < 1 || A.nt > 3 || M < 1 || M > 32 || K % kRowsKC)
     return launch_gemm(wt, epi, A, lda, W, M, N, K, C, ldc, H, ldh, st);
   const int nsplit = part && sync && fault ? gemm_rows_splits(M, N, K, part_floats) : 1;
 #define WICI_RW(NT_, TM_, E) \
-  gemm_rows_launch<NT_, TM_, E>(A, lda, W, M, N, K, nsplit, C, ldc, H, ldh, part, sync, fault, st)
+  gemm_rows_launch<NT_, TM_, E>(A, lda, W, M, N, K, nsplit, C, ldc, H, ldh, part, sync, fault, st, \
+                                drill)
 #define WICI_RW_NT(E)                                                        \
   switch (A.nt) {                                                            \
     case 1: return M <= 16 ? WICI_RW(1, 1, E) : WICI_RW(1, 2, E);            \

@@ -54,6 +54,7 @@ struct AttnFuse {
   void* state;
   float* out;
   int nsplit, n_heads, n_kv;
+  int drill;  // nonzero: report the splits as misplaced (tests of the error path)
 };
 int attn_fuse_ints(int n_kv);
 
@@ -205,13 +206,14 @@ int gemm_split_count(int wt, int nt, int M, int N, int K, int max_split);
 // every launch) and fault all non-null, products with few weight rows are split
 // along K and summed in the launch by the last split of each 64-row tile, all
 // splits of a tile on one XCD; *fault is set to 1 if they were not (the result
-// cannot be trusted then).  Launches that share sync must not overlap.
+// cannot be trusted then; with drill, every split-K sum reports so, for tests of
+// the error path).  Launches that share sync must not overlap.
 constexpr int kGemmRowsSyncInts = 512 * 64;
 int gemm_rows_splits(int M, int N, int K, size_t part_floats);
 hipError_t launch_gemm_rows(int wt, int epi, const ActBuf& A, int lda, const void* W, int M,
                             int N, int K, float* C, int ldc, const ActBuf& H, int ldh,
                             float* part, size_t part_floats, int* sync, int* fault,
-                            hipStream_t st);
+                            hipStream_t st, bool drill = false);
 // x[t] += sum over s < nsplit of P[s * p_split + t * d] (in that order) for T rows
 // of width d; then, with gain != nullptr, y[t] = RMSNorm(x[t]) * gain (as
 // launch_rmsnorm_rows).

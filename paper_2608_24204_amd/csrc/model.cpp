@@ -105,7 +105,7 @@ bool config_ok(const wici_config* c, std::string* why) {
   if (c->weight_dtype == WICI_F32 &&
       (c->d_model > 16384 || c->ffn_dim > 16384 || c->n_heads * c->head_dim > 16384))
     return bad("fp32 weights need d_model, ffn_dim and n_heads*head_dim of at most 16384");
-  if (c->flags & ~WICI_FLAG_NO_GRAPH) return bad("unknown flags");
+  if (c->flags & ~(WICI_FLAG_NO_GRAPH | WICI_FLAG_FAULT_DRILL)) return bad("unknown flags");
   if (c->prefill_planes != 0) {
     if (c->prefill_mode != WICI_PREFILL_BF16X3)
       return bad("prefill_planes needs prefill_mode WICI_PREFILL_BF16X3");
@@ -326,6 +326,7 @@ hipError_t enqueue_decode(wici_model* m, std::vector<wici::LaunchTimer>* timers 
   fuse.cnt = m->S<int>(L.attn_sync);
   fuse.xcc = fuse.cnt + c.n_kv_heads * 64;
   fuse.state = st;
+  fuse.drill = (c.flags & WICI_FLAG_FAULT_DRILL) != 0;
   // bf16 weights: the first QKV projection gathers the embedding row itself (its
   // profiling slot stays, at zero time)
   const bool fold_embed = wb == WICI_BF16;
@@ -506,7 +507,8 @@ hipError_t enqueue_decode_batch(wici_model* m, int B) {
   auto prod = [&](int epi, const wici::ActBuf& in, int K, size_t w, int N, float* out, int ldo,
                   const wici::ActBuf& hout, int ldh) {
     return wici::launch_gemm_rows(wb, epi, in, K, m->dw + w, B, N, K, out, ldo, hout, ldh,
-                                  gpart, gpart_floats, gsync, gfault, s);
+                                  gpart, gpart_floats, gsync, gfault, s,
+                                  (c.flags & WICI_FLAG_FAULT_DRILL) != 0);
   };
 #define WICI_TRY(call) \
   do {                 \

@@ -61,6 +61,18 @@ def test_invalid_config_is_rejected(field, value):
                                         ctypes.byref(sz)) == binding.WICI_E_ARG
 
 
+@pytest.mark.parametrize("flags", [binding.WICI_FLAG_NO_GRAPH, binding.WICI_FLAG_FAULT_DRILL,
+                                   binding.WICI_FLAG_NO_GRAPH | binding.WICI_FLAG_FAULT_DRILL])
+def test_known_flags_are_accepted(flags):
+    lib = binding.load_library()
+    c = _cfg()
+    c.flags = flags
+    sz = ctypes.c_size_t()
+    assert lib.wici_memory_requirements(ctypes.byref(c), ctypes.byref(sz), ctypes.byref(sz),
+                                        ctypes.byref(sz)) == binding.WICI_OK
+    assert binding.make_config(configs.TINY, fault_drill=True).flags == binding.WICI_FLAG_FAULT_DRILL
+
+
 @pytest.mark.parametrize("mode,planes,ok", [
     ("bf16x3", 0x9e, True), ("bf16x3", 0xff, True), ("bf16x3", 0x55, True),
     ("bf16x3", 0x9c, False), ("bf16x3", 0x29e, True), ("bf16x3", 0x455, False),

@@ -184,3 +184,29 @@ def test_batch_errors(cuda_ok):
     finally:
         for m in ms + [other]:
             m.close()
+
+
+def test_fault_drill_fails_the_batched_step(cuda_ok):
+    """WICI_FLAG_FAULT_DRILL on the lead: every split-K sum of the batched
+    products reports its splits as run on different XCDs, so the step fails
+    with WICI_E_HIP and the lead stays failed (the path a real misplacement
+    takes; the kernels run normally)."""
+    from paper_2608_24204_amd.binding import WICI_E_HIP, WICI_E_STATE, WiciError, WiciModel
+    cfg = CFGS["bf16"]
+    w = inputs.make_weights(cfg)
+    lead = WiciModel(cfg, max_seq=80, fault_drill=True)
+    ms = [lead]
+    try:
+        lead.load_weights(w)
+        ms.append(WiciModel(cfg, max_seq=80, share_weights_of=lead))
+        for m, p in zip(ms, prompts(cfg, 2)):
+            m.prefill(p)
+        with pytest.raises(WiciError) as e:
+            lead.decode_batch(ms)
+        assert e.value.status == WICI_E_HIP and "XCD" in str(e.value)
+        with pytest.raises(WiciError) as e:
+            lead.decode_batch(ms)
+        assert e.value.status == WICI_E_STATE
+    finally:
+        for m in ms:
+            m.close()

@@ -258,6 +258,28 @@ def test_split_prefill_equals_joint_prefill(cuda_ok):
     assert np.max(np.abs(l_joint - l_split)) / np.max(np.abs(l_joint)) < 1e-4
 
 
+@pytest.mark.parametrize("path", ["decode_step", "decode_n"])
+def test_fault_drill_fails_the_decode_step(cuda_ok, path):
+    """WICI_FLAG_FAULT_DRILL: the decode attention's merge in the last split block
+    reports its splits as run on different XCDs, so the step fails with
+    WICI_E_HIP and the model stays failed (the path a real misplacement takes;
+    the kernels run normally).  Prefill has no in-launch merge and succeeds."""
+    from paper_2608_24204_amd.binding import WICI_E_HIP, WICI_E_STATE, WiciError
+    cfg = SMALL["gqa128_bf16"]
+    w, _ = weights_for(cfg, 0.1)
+    m = make_model(cfg, w, fault_drill=True)
+    try:
+        m.prefill(inputs.make_prompt(cfg, 40))
+        with pytest.raises(WiciError) as e:
+            m.decode_step() if path == "decode_step" else m.decode_n(4)
+        assert e.value.status == WICI_E_HIP and "XCD" in str(e.value)
+        with pytest.raises(WiciError) as e:
+            m.decode_step()
+        assert e.value.status == WICI_E_STATE
+    finally:
+        m.close()
+
+
 def test_errors_and_state(cuda_ok):
     from paper_2608_24204_amd.binding import WiciError, WICI_E_ARG, WICI_E_CAPACITY, WICI_E_STATE
     cfg = SMALL["gqa64_bf16"]
