@@ -227,8 +227,8 @@ __global__ __launch_bounds__(256) void k_attn_decode(const float* __restrict__ q
 // the registers are held to 96 per lane, so five workgroups share a CU (the LDS
 // allows five): a long context's grid (8 KV heads x 129 splits at 8.2K
 // positions) then fits the chip in one round instead of leaving a tail.
-template <int HD, int G, bool FUSE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G <= 5 && !FUSE ? 5 : 1))) void
+template <int HD, int G, bool FUSE, bool ROPE = false>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(G <= 5 && !FUSE ? (ROPE ? 4 : 5) : 1))) void
 k_attn_decode_mfma(const float* __restrict__ q_in,
                    KvLayout kv,
                    const DecodeState* __restrict__ st,
@@ -237,7 +237,8 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
                    const SeqDesc* __restrict__ seqs,
                    int layer,
                    int q_stride,
-                   AttnFuse fz) {
+                   AttnFuse fz,
+                   RopeIn rope) {
   static_assert(G <= 16, "query heads are the 16 columns of a tile");
   static_assert(!FUSE || G * HD <= 512, "the merge holds at most 16 partials per thread");
   if (seqs) {
@@ -267,7 +268,7 @@ k_attn_decode_mfma(const float* __restrict__ q_in,
     split = blockIdx.x;
     g = blockIdx.y;
   }
-  const int n = attn_split_mfma<HD, G>(q_in, kv, st, part_o, part_ml, g, split, nsplit);
+  const int n = attn_split_mfma<HD, G, ROPE>(q_in, kv, st, part_o, part_ml, g, split, nsplit, rope);
   if constexpr (FUSE)
     if (n > 0) attn_merge_in_last_split<HD, G>(fz, g, split, nsplit, n, part_o, part_ml);
 }
@@ -462,7 +463,7 @@ static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const Decod
       fz.n_kv = kv.n_kv;
       const int blocks = 8 * ((kv.n_kv + 7) / 8) * nsplit;
       launch_k(k_attn_decode_mfma<HD, G, true>, dim3(blocks), dim3(256), 0, s, kOnly, q, kv, st,
-               part_o, part_ml, (const SeqDesc*)nullptr, 0, 0, fz);
+               part_o, part_ml, (const SeqDesc*)nullptr, 0, 0, fz, RopeIn{});
       return hipGetLastError();
     }
     // longer: splits of several sub-chunks, as few as keep them within the merge
@@ -483,7 +484,7 @@ static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const Decod
   }
   if constexpr (sizeof(KT) == 2)
     launch_k(k_attn_decode_mfma<HD, G, false>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q,
-             kv, st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0, AttnFuse{});
+             kv, st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0, AttnFuse{}, RopeIn{});
   else
     launch_k(k_attn_decode<HD, KT, G>, dim3(nsplit, kv.n_kv), dim3(256), 0, s, kFirst, q, kv,
              st, part_o, part_ml, (const SeqDesc*)nullptr, 0, 0);
@@ -499,12 +500,19 @@ static hipError_t attn_decode_t(const float* q, int Hq, KvLayout kv, const Decod
 template <int HD, typename KT, int G>
 static hipError_t attn_decode_batch_t(const float* q, int q_stride, int B, int Hq, KvLayout kv,
                                       const SeqDesc* seqs, int layer, int nsplit, float* part_o,
-                                      float* part_ml, const ActBuf& out, hipStream_t s) {
-  if constexpr (sizeof(KT) == 2)
-    hipLaunchKernelGGL((k_attn_decode_mfma<HD, G, false>), dim3(nsplit, kv.n_kv, B), dim3(256), 0,
-                       s, q, kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer,
-                       q_stride, AttnFuse{});
-  else
+                                      float* part_ml, const ActBuf& out, hipStream_t s,
+                                      const RopeIn* rope) {
+  if (rope && sizeof(KT) != 2) return hipErrorInvalidValue;
+  if constexpr (sizeof(KT) == 2) {
+    if (rope)
+      hipLaunchKernelGGL((k_attn_decode_mfma<HD, G, false, true>), dim3(nsplit, kv.n_kv, B),
+                         dim3(256), 0, s, q, kv, (const DecodeState*)nullptr, part_o, part_ml,
+                         seqs, layer, q_stride, AttnFuse{}, *rope);
+    else
+      hipLaunchKernelGGL((k_attn_decode_mfma<HD, G, false>), dim3(nsplit, kv.n_kv, B), dim3(256),
+                         0, s, q, kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer,
+                         q_stride, AttnFuse{}, RopeIn{});
+  } else
     hipLaunchKernelGGL((k_attn_decode<HD, KT, G>), dim3(nsplit, kv.n_kv, B), dim3(256), 0, s, q,
                        kv, (const DecodeState*)nullptr, part_o, part_ml, seqs, layer, q_stride);
   hipLaunchKernelGGL((k_attn_merge_batch<HD>), dim3(Hq, B), dim3(HD), 0, s, part_o, part_ml,
@@ -530,9 +538,9 @@ template <int HD, typename KT>
 static hipError_t attn_decode_batch_g(int G, const float* q, int q_stride, int B, int Hq,
                                       KvLayout kv, const SeqDesc* seqs, int layer, int nsplit,
                                       float* part_o, float* part_ml, const ActBuf& out,
-                                      hipStream_t s) {
+                                      hipStream_t s, const RopeIn* rope) {
 #define WICI_B(GG) \
-  case GG: return attn_decode_batch_t<HD, KT, GG>(q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s)
+  case GG: return attn_decode_batch_t<HD, KT, GG>(q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s, rope)
   switch (G) {
     WICI_B(1); WICI_B(2); WICI_B(4); WICI_B(5); WICI_B(8);
     default: return hipErrorInvalidValue;
@@ -543,18 +551,18 @@ static hipError_t attn_decode_batch_g(int G, const float* q, int q_stride, int B
 hipError_t launch_attn_decode_batch(bool kv_bf16, const float* q, int q_stride, int B, int Hq,
                                     KvLayout kv, const SeqDesc* seqs, int layer, int nsplit,
                                     float* part_o, float* part_ml, const ActBuf& out,
-                                    hipStream_t s) {
+                                    hipStream_t s, const RopeIn* rope) {
   if (B < 1 || nsplit > kMaxSplits || nsplit * kChunk < kv.max_pos || kv.n_kv < 1 ||
       Hq % kv.n_kv || kv.page < 1 || (kv.page & (kv.page - 1)))
     return hipErrorInvalidValue;
   const int G = Hq / kv.n_kv;
   if (kv.hd == 128) {
-    if (kv_bf16) return attn_decode_batch_g<128, bf16_t>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s);
-    return attn_decode_batch_g<128, float>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s);
+    if (kv_bf16) return attn_decode_batch_g<128, bf16_t>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s, rope);
+    return attn_decode_batch_g<128, float>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s, rope);
   }
   if (kv.hd == 64) {
-    if (kv_bf16) return attn_decode_batch_g<64, bf16_t>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s);
-    return attn_decode_batch_g<64, float>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s);
+    if (kv_bf16) return attn_decode_batch_g<64, bf16_t>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s, rope);
+    return attn_decode_batch_g<64, float>(G, q, q_stride, B, Hq, kv, seqs, layer, nsplit, part_o, part_ml, out, s, rope);
   }
   return hipErrorInvalidValue;
 }

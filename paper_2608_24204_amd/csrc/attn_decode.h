@@ -133,12 +133,22 @@ __device__ __forceinline__ void attn_merge_in_last_split(const AttnFuse& fz, int
 // (max, sum) statistics into part_o / part_ml ([Hq][nsplit] order) and returns
 // the context length n = pos + 1, or 0 when the split lies past the context
 // (nothing is written then).  Called by whole 256-thread workgroups.
-template <int HD, int G>
+//
+// With ROPE (the batched step), q_in is the sequence's raw projection row
+// (query heads, key heads, value heads) and this launch does the work of the
+// RoPE + append kernel it replaces: every split rotates its query at the
+// position (and scales it by rope.q_scale), and the split holding the position
+// rotates that position's key, rounds key and value to the cache type, uses
+// them for its own scores and stores them in the cache.  A lane's dimensions
+// 32 s + 8 (l / 16) + e hold both members of each RoPE pair (j, j + HD / 2):
+// steps s and s + DS / 2.
+
+template <int HD, int G, bool ROPE = false>
 __device__ __forceinline__ int attn_split_mfma(const float* __restrict__ q_in, const KvLayout& kv,
                                                const DecodeState* __restrict__ st,
                                                float* __restrict__ part_o,
                                                float* __restrict__ part_ml, int g, int split,
-                                               int nsplit) {
+                                               int nsplit, RopeIn rope = RopeIn{}) {
   constexpr int DS = HD / 32;  // 32-deep steps of S^T
   constexpr int DT = HD / 16;  // 16-wide output tiles of P V
   constexpr int VP = 16 + 4;   // LDS row of one dimension's 16 positions (8-byte aligned reads)
@@ -185,6 +195,49 @@ __device__ __forceinline__ int attn_split_mfma(const float* __restrict__ q_in, c
   for (int s = 0; s < DS; ++s) {
     kf[s] = *reinterpret_cast<const bf16x8_t*>(pk + 32 * s);
     vr[s] = *reinterpret_cast<const uint4*>(pv + 32 * s);
+  }
+  if constexpr (ROPE) {
+    constexpr int H2 = DS / 2;  // steps holding the first member of a pair
+    const int pos = n - 1;
+    const float* cr = rope.cos + (size_t)pos * (HD / 2) + 8 * g4;
+    const float* sr = rope.sin + (size_t)pos * (HD / 2) + 8 * g4;
+    // the query, rotated and scaled
+#pragma unroll
+    for (int s = 0; s < H2; ++s)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float a = qv[s][e], bb = qv[s + H2][e], c = cr[32 * s + e], sn = sr[32 * s + e];
+        const float ra = a * c - bb * sn, rb = a * sn + bb * c;
+        qv[s][e] = ra * rope.q_scale;
+        qv[s + H2][e] = rb * rope.q_scale;
+      }
+    // the new position's key (rotated) and value, from the projection row
+    if (jl == pos) {
+      const float* kr = q_in + ((size_t)Hkv * G + g) * HD + 8 * g4;
+      const float* vrow = q_in + ((size_t)Hkv * G + Hkv + g) * HD + 8 * g4;
+#pragma unroll
+      for (int s = 0; s < H2; ++s)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float a = kr[32 * s + e], bb = kr[32 * (s + H2) + e];
+          const float c = cr[32 * s + e], sn = sr[32 * s + e];
+          kf[s][e] = static_cast<__bf16>(a * c - bb * sn);
+          kf[s + H2][e] = static_cast<__bf16>(a * sn + bb * c);
+        }
+#pragma unroll
+      for (int s = 0; s < DS; ++s) {
+        unsigned w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          w[e] = (unsigned)f32_to_bf16(vrow[32 * s + 2 * e]) |
+                 ((unsigned)f32_to_bf16(vrow[32 * s + 2 * e + 1]) << 16);
+        vr[s] = make_uint4(w[0], w[1], w[2], w[3]);
+        bf16_t* wk = const_cast<bf16_t*>(pk) + 32 * s;
+        bf16_t* wv = const_cast<bf16_t*>(pv) + 32 * s;
+        *reinterpret_cast<bf16x8_t*>(wk) = kf[s];
+        *reinterpret_cast<uint4*>(wv) = vr[s];
+      }
+    }
   }
   // the query as three bf16 terms (columns past G are zero)
   bf16x8_t qb[3][DS];

@@ -146,13 +146,23 @@ hipError_t launch_rope_append_batch(bool kv_bf16, float* qkv, int B, int Hq, con
 // (a row with a non-finite logit gets token -1 and the failed flag).
 hipError_t launch_argmax_rows(const float* logits, int B, int V, const SeqDesc* seqs,
                               hipStream_t st);
+// RoPE tables and the query scale, for a decode attention that applies RoPE and
+// appends the new key and value itself.
+struct RopeIn {
+  const float* cos;  // [max_seq][hd / 2]
+  const float* sin;
+  float q_scale;
+};
 // Batched decode attention: row b's queries (q + b * q_stride, rotated and scaled)
 // over sequence b's cache [0, pos_b]; partials [B][Hq][nsplit]; out is the
-// activation buffer of the O projection, row b at b * Hq * hd.
+// activation buffer of the O projection, row b at b * Hq * hd.  With rope (bf16
+// caches only) row b is instead the raw projection row (query, key, value
+// heads): the launch rotates and scales the queries and rotates and appends the
+// position's key and value itself, in place of launch_rope_append_batch.
 hipError_t launch_attn_decode_batch(bool kv_bf16, const float* q, int q_stride, int B, int Hq,
                                     KvLayout kv, const SeqDesc* seqs, int layer, int nsplit,
                                     float* part_o, float* part_ml, const ActBuf& out,
-                                    hipStream_t st);
+                                    hipStream_t st, const RopeIn* rope = nullptr);
 
 // Prefill: rotate q (in place) and k of T rows at positions p0..p0+T-1 and
 // append k, v to the cache.  qkv rows are [Hq*hd | Hkv*hd | Hkv*hd] fp32.

@@ -29,6 +29,7 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kMaxGemvBlocks = 1024;
 constexpr int kMaxBatch = 256;  // sequences per batched decode step
+constexpr size_t kFuseRopeMaxBlocks = 3 * 4 * 256;  // see enqueue_decode_batch
 constexpr int kMaxKSplit = 4;   // K ranges of a prefill residual product (partials kept)
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
@@ -496,6 +497,13 @@ hipError_t enqueue_decode_batch(wici_model* m, int B) {
   float* logits = m->S<float>(L.h);
   wici::KvLayout kv = m->kv(0);  // geometry; pool and table come per sequence
   const float q_scale = 1.0f / std::sqrt((float)c.head_dim);
+  const wici::RopeIn rope{m->W<float>(L.rope_cos), m->W<float>(L.rope_sin), q_scale};
+  // A bf16 cache: the attention can apply RoPE and append the position itself
+  // (one launch fewer per layer), but its registers then allow four workgroups
+  // per CU instead of five.  Measured (8B, 21 splits): B = 2, 4, 8 +4%, +4%,
+  // +2%, B = 16 even, B = 32 -2%; so only while its grid is at most about three
+  // rounds of the chip at that occupancy.
+  const bool fuse_rope = kb && (size_t)L.nsplit * c.n_kv_heads * B <= kFuseRopeMaxBlocks;
   hipStream_t s = m->stream;
   hipError_t e;
   // the products: split-K partials in the prefill's split buffer, a misplaced
@@ -522,10 +530,11 @@ hipError_t enqueue_decode_batch(wici_model* m, int B) {
                                        a, s));
     WICI_TRY(prod(wici::GEMV_STORE, rd(a, pl.qkv), d, m->layer(l, L.l_wqkv), nqkv, qkv, nqkv,
                   none, 0));
-    WICI_TRY(wici::launch_rope_append_batch(kb, qkv, B, c.n_heads, m->W<float>(L.rope_cos),
-                                            m->W<float>(L.rope_sin), seqs, l, kv, q_scale, s));
+    if (!fuse_rope)
+      WICI_TRY(wici::launch_rope_append_batch(kb, qkv, B, c.n_heads, m->W<float>(L.rope_cos),
+                                              m->W<float>(L.rope_sin), seqs, l, kv, q_scale, s));
     WICI_TRY(wici::launch_attn_decode_batch(kb, qkv, nqkv, B, c.n_heads, kv, seqs, l, L.nsplit,
-                                            part_o, part_ml, att, s));
+                                            part_o, part_ml, att, s, fuse_rope ? &rope : nullptr));
     WICI_TRY(prod(wici::GEMV_RESID, rd(att, pl.o), qd, m->layer(l, L.l_wo), d, x, d, none, 0));
     WICI_TRY(wici::launch_rmsnorm_rows(x, m->W<float>(m->layer(l, L.l_fnorm)), c.rms_eps, B, d,
                                        a, s));

@@ -72,18 +72,21 @@ def test_batched_decode_matches_oracle_per_sequence(cuda_ok, kind, cap):
         assert rep.strict_ids, rep.summary()
 
 
-@pytest.mark.parametrize("n", [20, 33])
-def test_large_batches_match_oracle(cuda_ok, n):
+@pytest.mark.parametrize("n,cap", [(20, 140), (33, 140), (8, 16384)])
+def test_large_batches_match_oracle(cuda_ok, n, cap):
     """17-32 sequences: the batched products take the rows in two 16-row tiles
     (split along K for the projections with few weight rows, summed in the
-    launch); past 32 they are the prefill's matrix-core products."""
+    launch); past 32 they are the prefill's matrix-core products.  8 sequences
+    at a 16384-position capacity (256 splits): the attention grid is past the
+    size where the attention applies RoPE and appends itself, so the separate
+    RoPE + append pass runs."""
     cfg = CFGS["bf16"]
     w = inputs.make_weights(cfg, gain_std=0.1)
     w64 = inputs.weights_f64(cfg, w)
     steps = 5
     rng = np.random.default_rng(11)
     ps = [rng.integers(0, cfg.vocab, 20 + 3 * b).astype(np.int32) for b in range(n)]
-    ms = clients(cfg, w, n, kv_page=16, max_seq=140)
+    ms = clients(cfg, w, n, kv_page=16, max_seq=cap)
     try:
         ids = [[m.prefill(p)[0]] for m, p in zip(ms, ps)]
         logs = [[] for _ in range(n)]
