@@ -213,3 +213,47 @@ def test_fault_drill_fails_the_batched_step(cuda_ok):
     finally:
         for m in ms:
             m.close()
+
+
+GROUP_CFGS = {
+    "hd64_g4": configs.ModelConfig(name="t_batch_hd64", key=97, n_layers=2, d_model=512, n_heads=8,
+                                   n_kv_heads=2, head_dim=64, ffn_dim=1024, vocab=1500,
+                                   prompt_len=40, decode_steps=6, rope_base=500000.0),
+    "hd128_g5": configs.ModelConfig(name="t_batch_g5", key=98, n_layers=2, d_model=640,
+                                    n_heads=10, n_kv_heads=2, head_dim=128, ffn_dim=1536,
+                                    vocab=1531, prompt_len=40, decode_steps=6, rope_base=1e6),
+    "hd128_g8": configs.ModelConfig(name="t_batch_g8", key=99, n_layers=2, d_model=512,
+                                    n_heads=16, n_kv_heads=2, head_dim=128, ffn_dim=1024,
+                                    vocab=1700, prompt_len=40, decode_steps=6),
+}
+
+
+@pytest.mark.parametrize("name", list(GROUP_CFGS))
+def test_batched_attention_shapes_match_oracle(cuda_ok, name):
+    """The batched attention with its own RoPE + append at head dimension 64
+    (each RoPE pair in one lane's steps 0 and 1) and with 5 and 8 query heads
+    per KV head."""
+    cfg = GROUP_CFGS[name]
+    w = inputs.make_weights(cfg, gain_std=0.1)
+    w64 = inputs.weights_f64(cfg, w)
+    n = 3
+    rng = np.random.default_rng(5)
+    ps = [rng.integers(0, cfg.vocab, cfg.prompt_len - 7 * b).astype(np.int32) for b in range(n)]
+    ms = clients(cfg, w, n, kv_page=16, max_seq=cfg.prompt_len + cfg.decode_steps + 2)
+    try:
+        ids = [[m.prefill(p)[0]] for m, p in zip(ms, ps)]
+        logs = [[] for _ in range(n)]
+        for _ in range(cfg.decode_steps):
+            toks, lg = ms[0].decode_batch(ms, want_logits=True)
+            for b in range(n):
+                ids[b].append(int(toks[b]))
+                logs[b].append(lg[b])
+    finally:
+        for m in ms:
+            m.close()
+    for b in range(n):
+        ora_ids, ora = oracle_run(cfg, w64, ps[b], cfg.decode_steps)
+        rep = compare(ids[b], [None] + logs[b], ora_ids, ora)
+        print(f"[batch] {name} seq {b} (P={len(ps[b])}): {rep.summary()}", flush=True)
+        assert rep.max_rel_err <= 2e-2
+        assert rep.strict_ids, rep.summary()
