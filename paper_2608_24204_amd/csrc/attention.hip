@@ -595,15 +595,17 @@ int attn_fuse_ints(int n_kv) { return 2 * n_kv * kFuseLine; }
 // ------------------------------------------------------------------- prefill
 template <int HD, typename KT>
 __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ qkv, int T,
-                                                      int p0, int Hq, KvLayout kv, ActBuf out) {
+                                                      int p0, int Hq, KvLayout kv, ActBuf out,
+                                                      int cus) {
   constexpr int BQ = 64, BKEY = 64, DPT = HD / 4;
   __shared__ float Ks[BKEY][HD + 4];
   __shared__ float Vs[BKEY][HD + 4];
-  // the second half of the heads takes the query blocks in reverse order: the
-  // grid is dealt out in order, workgroups b and b + (grid / 2) share a CU when
-  // two fit, and the causal walk of block i is i + 1 key blocks, so this pairs
-  // long walks with short ones on every CU
-  const int qbi = blockIdx.y >= (gridDim.y + 1) / 2 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+  // the grid is dealt out in order, one workgroup per CU and then a second, so
+  // workgroups b and b + (CUs) share a CU, and the causal walk of query block i
+  // is i + 1 key blocks: alternate runs of `cus` workgroups take the query
+  // blocks in reverse order, pairing long walks with short ones on every CU
+  const int lin = blockIdx.x + gridDim.x * blockIdx.y;
+  const int qbi = (lin / cus) & 1 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
   const int qb = qbi * BQ, h = blockIdx.y;
   const int Hkv = kv.n_kv, g = h / (Hq / Hkv);
   const int tid = threadIdx.x, ql = tid >> 2, part = tid & 3;
@@ -686,18 +688,19 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
 template <int HD, int NT>
 __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restrict__ qkv, int T,
                                                            int p0, int Hq, KvLayout kv,
-                                                           ActBuf out) {
+                                                           ActBuf out, int cus) {
   constexpr int BQ = 64, BKEY = 64, KP = HD + 8, VP = BKEY + 8;
   constexpr int DS = HD / 32;   // 32-deep steps over the head dimension
   constexpr int DT = HD / 16;   // 16-wide output column tiles
   __shared__ __attribute__((aligned(16))) bf16_t Ks[BKEY][KP];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[HD][VP];
 
-  // the second half of the heads takes the query blocks in reverse order: the
-  // grid is dealt out in order, workgroups b and b + (grid / 2) share a CU when
-  // two fit, and the causal walk of block i is i + 1 key blocks, so this pairs
-  // long walks with short ones on every CU
-  const int qbi = blockIdx.y >= (gridDim.y + 1) / 2 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+  // the grid is dealt out in order, one workgroup per CU and then a second, so
+  // workgroups b and b + (CUs) share a CU, and the causal walk of query block i
+  // is i + 1 key blocks: alternate runs of `cus` workgroups take the query
+  // blocks in reverse order, pairing long walks with short ones on every CU
+  const int lin = blockIdx.x + gridDim.x * blockIdx.y;
+  const int qbi = (lin / cus) & 1 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
   const int qb = qbi * BQ, h = blockIdx.y;
   const int Hkv = kv.n_kv, g = h / (Hq / Hkv);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -886,11 +889,27 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   }
 }
 
+// Compute units of the current device (the prefill attention's workgroup
+// pairing), looked up once per device.
+static int device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        v < 1)
+      v = 256;
+    cached[dev] = v;
+  }
+  return cached[dev];
+}
+
 template <int HD, typename KT>
 static hipError_t attn_prefill_t(const float* qkv, int T, int p0, int Hq, KvLayout kv,
                                  const ActBuf& out, hipStream_t s) {
   hipLaunchKernelGGL((k_attn_prefill<HD, KT>), dim3((T + 63) / 64, Hq), dim3(256), 0, s, qkv, T,
-                     p0, Hq, kv, out);
+                     p0, Hq, kv, out, device_cus());
   return hipGetLastError();
 }
 
@@ -898,10 +917,11 @@ template <int HD>
 static hipError_t attn_prefill_mfma(const float* qkv, int T, int p0, int Hq, KvLayout kv,
                                     const ActBuf& out, int terms, hipStream_t s) {
   const dim3 grid((T + 63) / 64, Hq);
+  const int cus = device_cus();
   switch (terms) {
-    case 1: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 1>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
-    case 2: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 2>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
-    case 3: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 3>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out); break;
+    case 1: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 1>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out, cus); break;
+    case 2: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 2>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out, cus); break;
+    case 3: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 3>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out, cus); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
