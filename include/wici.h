@@ -264,8 +264,9 @@ wici_status wici_read_kv(wici_model* m, int32_t layer, int32_t begin, int32_t en
  * entries) and their number (3 + 5 * n_layers) to *n_written.  Order: embedding
  * (0 with bf16 weights, whose first QKV GEMV gathers the embedding row itself);
  * per layer: QKV GEMV (with RoPE and the KV append), attention (with a bf16
- * cache and at most 32 splits one launch that also merges the splits, else
- * split pass start to merge end), O GEMV, gate/up GEMV, down GEMV; then the LM
+ * cache and up to 4 query heads of 128 or 8 of 64 per KV head, one launch that
+ * also merges the splits; otherwise split pass start to merge end), O GEMV,
+ * gate/up GEMV, down GEMV; then the LM
  * head GEMV and the final argmax.  Errors as wici_decode_step, plus WICI_E_ARG
  * for NULL outputs or a capacity below 3 + 5 * n_layers. */
 wici_status wici_profile_decode_step(wici_model* m, int32_t token_in, int32_t* next_token,
