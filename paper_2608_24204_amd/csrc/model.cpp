@@ -418,10 +418,12 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T, int tok_off) {
                                          std::min(kMaxKSplit, kMaxKSplit * d / nqkv));
   const size_t q_split = C * nqkv;
   int pending = 0;  // splits of the previous down product not yet added to x
-  auto norm = [&](const float* gain, int nsplit) {
+  // (the normalised rows are written with as many terms as their product reads)
+  auto norm = [&](const float* gain, int nsplit, int terms) {
+    const wici::ActBuf y = rd(a, terms);
     return nsplit > 1 ? wici::launch_resid_sum_rmsnorm(x, P, nsplit, p_split, gain, c.rms_eps, T,
-                                                       d, a, s)
-                      : wici::launch_rmsnorm_rows(x, gain, c.rms_eps, T, d, a, s);
+                                                       d, y, s)
+                      : wici::launch_rmsnorm_rows(x, gain, c.rms_eps, T, d, y, s);
   };
   auto resid = [&](const wici::ActBuf& in, int K, size_t w, int nsplit) {
     return nsplit > 1 ? wici::launch_gemm_split(wb, in, K, m->dw + w, T, d, K, nsplit, P, p_split,
@@ -430,7 +432,7 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T, int tok_off) {
                                           none, 0, s);
   };
   for (int l = 0; l < c.n_layers; ++l) {
-    if ((e = norm(m->W<float>(m->layer(l, L.l_anorm)), pending))) return e;
+    if ((e = norm(m->W<float>(m->layer(l, L.l_anorm)), pending, pl.qkv))) return e;
     if (s_q > 1) {
       if ((e = wici::launch_gemm_split(wb, rd(a, pl.qkv), d, m->dw + m->layer(l, L.l_wqkv), T,
                                        nqkv, d, s_q, P, q_split, s)))
@@ -447,7 +449,7 @@ hipError_t enqueue_prefill_chunk(wici_model* m, int p0, int T, int tok_off) {
     if ((e = wici::launch_attn_prefill(kb, qkv, T, p0, c.n_heads, m->kv(l), att, s, pl.attn)))
       return e;
     if ((e = resid(rd(att, pl.o), qd, m->layer(l, L.l_wo), s_o))) return e;
-    if ((e = norm(m->W<float>(m->layer(l, L.l_fnorm)), s_o))) return e;
+    if ((e = norm(m->W<float>(m->layer(l, L.l_fnorm)), s_o, pl.gu))) return e;
     if ((e = wici::launch_gemm(wb, wici::GEMV_SWIGLU, rd(a, pl.gu), d,
                                m->dw + m->layer(l, L.l_wgu), T, 2 * F, d, nullptr, 0, h, F, s)))
       return e;
