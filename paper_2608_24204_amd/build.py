@@ -32,6 +32,13 @@ FLAGS = [
 ]
 
 
+# Per-source flags.  attention.hip: matrix-core results in ordinary vector
+# registers (not the accumulation registers), so the flash-attention loop's
+# rescaled output rows are not copied between the two register files on every
+# key block.
+EXTRA = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -51,7 +58,7 @@ def build(verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         lang = ["-x", "hip"]
-        cmds.append([HIPCC, *lang, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([HIPCC, *lang, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     jobs = min(len(cmds), max(1, min(16, os.cpu_count() or 1)))
     with ThreadPoolExecutor(jobs) as ex:

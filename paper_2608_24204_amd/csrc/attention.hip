@@ -12,6 +12,8 @@
 // Prefill: one block per (64 queries, query head), keys streamed through LDS in
 // blocks of 64 with an online softmax; on the matrix cores for a bf16 cache (the
 // fp32 query and probabilities split into bf16 terms), else fp32 vector code.
+#include <type_traits>
+
 #include "attn_decode.h"
 #include "common.h"
 #include "kernels.h"
@@ -602,11 +604,13 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
   __shared__ float Vs[BKEY][HD + 4];
   // the grid is dealt out in order, one workgroup per CU and then a second, so
   // workgroups b and b + (CUs) share a CU, and the causal walk of query block i
-  // is i + 1 key blocks: alternate runs of `cus` workgroups take the query
-  // blocks in reverse order, pairing long walks with short ones on every CU
-  const int lin = blockIdx.x + gridDim.x * blockIdx.y;
-  const int qbi = (lin / cus) & 1 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
-  const int qb = qbi * BQ, h = blockIdx.y;
+  // is i + 1 key blocks: alternate runs of heads, each run as many heads as
+  // (CUs) workgroups hold, take their query blocks in reverse order, pairing
+  // long walks with short ones on every CU (the order is a function of the head
+  // alone, so every (head, query block) is taken exactly once)
+  const int h = blockIdx.y, run = max(1, cus / (int)gridDim.x);
+  const int qbi = (h / run) & 1 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+  const int qb = qbi * BQ;
   const int Hkv = kv.n_kv, g = h / (Hq / Hkv);
   const int tid = threadIdx.x, ql = tid >> 2, part = tid & 3;
   const int t = qb + ql;
@@ -689,19 +693,35 @@ template <int HD, int NT>
 __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restrict__ qkv, int T,
                                                            int p0, int Hq, KvLayout kv,
                                                            ActBuf out, int cus) {
-  constexpr int BQ = 64, BKEY = 64, KP = HD + 8, VP = BKEY + 8;
+  // V^T rows of 68 bf16 (34 dwords), key pairs XOR-swizzled by row group (see
+  // vt_col): the transposing 4-byte stores of a wavefront land on 64 distinct
+  // banks (8 rows x 8 pairs per store instruction otherwise share 8 banks)
+  constexpr int BQ = 64, BKEY = 64, KP = HD + 8, VP = BKEY + 4;
   constexpr int DS = HD / 32;   // 32-deep steps over the head dimension
   constexpr int DT = HD / 16;   // 16-wide output column tiles
   __shared__ __attribute__((aligned(16))) bf16_t Ks[BKEY][KP];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[HD][VP];
+  // element column of key pair kp in V^T row group rg (rows 16 rg .. 16 rg + 15)
+  auto vt_col = [](int rg, int kp) { return 2 * (kp ^ (8 * ((rg >> 1) & 3))); };
 
-  // the grid is dealt out in order, one workgroup per CU and then a second, so
-  // workgroups b and b + (CUs) share a CU, and the causal walk of query block i
-  // is i + 1 key blocks: alternate runs of `cus` workgroups take the query
-  // blocks in reverse order, pairing long walks with short ones on every CU
-  const int lin = blockIdx.x + gridDim.x * blockIdx.y;
-  const int qbi = (lin / cus) & 1 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
-  const int qb = qbi * BQ, h = blockIdx.y;
+  // A 1-D grid of (query block, head) pairs, padded to a multiple of 8.
+  // Workgroups are dealt to the 8 XCDs in turn, so those of one index mod 8
+  // share an XCD's L2: each such class takes a contiguous range of the pairs,
+  // head-major, which keeps the query heads of a KV head (and so its keys and
+  // values) on one XCD.  The grid is dealt out one workgroup per CU and then a
+  // second, so workgroups b and b + (CUs) share a CU; their pairs lie CUs / 8
+  // apart.  The causal walk of query block i is i + 1 key blocks, so alternate
+  // runs of heads, each run as long as that distance, take their query blocks
+  // in reverse order, pairing long walks with short ones on every CU.  The
+  // order is a function of the head alone, so every (head, query block) is
+  // still taken exactly once.
+  const int nqb = (T + BQ - 1) / BQ;
+  const int lin = blockIdx.x, pair = (lin % 8) * (gridDim.x / 8) + lin / 8;
+  if (pair >= nqb * Hq) return;
+  const int h = pair / nqb, qq = pair % nqb;
+  const int run = max(1, cus / 8 / nqb);  // heads per run
+  const int qbi = (h / run) & 1 ? nqb - 1 - qq : qq;
+  const int qb = qbi * BQ;
   const int Hkv = kv.n_kv, g = h / (Hq / Hkv);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int l16 = lane & 15, lg = lane >> 4;
@@ -737,57 +757,54 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
 
   // ---- key/value loading: thread -> (key pair, 16-wide column chunk) --------------
   constexpr int NCH = HD / 16;                // column chunks per key
-  constexpr int PAIRS = BKEY / 2;
-  constexpr int ITEMS = PAIRS * NCH;          // (pair, chunk) items per block
-  constexpr int PER = (ITEMS + 255) / 256;
-  uint4 rk[PER][2][2], rv[PER][2][2];         // [item][key of pair][16-byte half]
+  constexpr int ITEMS = BKEY / 2 * NCH;       // (pair, chunk) items per block
+  static_assert(ITEMS <= 256, "one (pair, chunk) item per thread at most");
+  const bool has_item = tid < ITEMS;
+  const int pr = min(tid, ITEMS - 1) / NCH, ch = min(tid, ITEMS - 1) % NCH;
+  uint4 k0a, k0b, k1a, k1b, v0a, v0b, v1a, v1b;  // the pair's keys 0/1, 16-byte halves a/b
   const int kend = p0 + min(T, qb + BQ);      // keys [0, kend) are visible to this block
+  // Every load is unconditional, keys past the visible range clamped to the
+  // last visible one (finite values that the mask gives zero weight): a load
+  // under a branch makes the compiler wait for every load in flight where the
+  // paths join, which would expose each block's load latency.  The physical
+  // pages of a block's keys are requested one block before its keys and
+  // values, which keeps the page lookup off their path.
+  int pt0, pt1;
+  auto tload = [&](int kb) {
+    pt0 = kv.table[min(kb + 2 * pr, kend - 1) >> ps];
+    pt1 = kv.table[min(kb + 2 * pr + 1, kend - 1) >> ps];
+  };
+  const bf16_t* kbase = base + (size_t)g * head_stride + ch * 16;
+  const size_t pstride = (size_t)2 * Hkv * head_stride;  // elements per physical page
+  const size_t vofs = (size_t)Hkv * head_stride;         // values after the keys
   auto gload = [&](int kb) {
-#pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      const int item = tid + it * 256;
-      if (item < ITEMS) {
-        const int pr = item / NCH, ch = item % NCH;
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int j = kb + 2 * pr + u;
-          if (j < kend) {
-            const int pp = kv.table[j >> ps];
-            const bf16_t* kp = base + (((size_t)pp * 2 + 0) * Hkv + g) * head_stride +
-                               (size_t)(j & (kv.page - 1)) * HD + ch * 16;
-            const bf16_t* vp = kp + (size_t)Hkv * head_stride;
-            rk[it][u][0] = *reinterpret_cast<const uint4*>(kp);
-            rk[it][u][1] = *reinterpret_cast<const uint4*>(kp + 8);
-            rv[it][u][0] = *reinterpret_cast<const uint4*>(vp);
-            rv[it][u][1] = *reinterpret_cast<const uint4*>(vp + 8);
-          } else {
-            rk[it][u][0] = rk[it][u][1] = rv[it][u][0] = rv[it][u][1] = make_uint4(0, 0, 0, 0);
-          }
-        }
-      }
-    }
+    const int j0 = min(kb + 2 * pr, kend - 1), j1 = min(kb + 2 * pr + 1, kend - 1);
+    const bf16_t* kp0 = kbase + (size_t)pt0 * pstride + (size_t)(j0 & (kv.page - 1)) * HD;
+    const bf16_t* kp1 = kbase + (size_t)pt1 * pstride + (size_t)(j1 & (kv.page - 1)) * HD;
+    k0a = *reinterpret_cast<const uint4*>(kp0);
+    k0b = *reinterpret_cast<const uint4*>(kp0 + 8);
+    k1a = *reinterpret_cast<const uint4*>(kp1);
+    k1b = *reinterpret_cast<const uint4*>(kp1 + 8);
+    v0a = *reinterpret_cast<const uint4*>(kp0 + vofs);
+    v0b = *reinterpret_cast<const uint4*>(kp0 + vofs + 8);
+    v1a = *reinterpret_cast<const uint4*>(kp1 + vofs);
+    v1b = *reinterpret_cast<const uint4*>(kp1 + vofs + 8);
   };
   auto sstore = [&]() {
+    if (has_item) {
+      *reinterpret_cast<uint4*>(&Ks[2 * pr][ch * 16]) = k0a;
+      *reinterpret_cast<uint4*>(&Ks[2 * pr][ch * 16 + 8]) = k0b;
+      *reinterpret_cast<uint4*>(&Ks[2 * pr + 1][ch * 16]) = k1a;
+      *reinterpret_cast<uint4*>(&Ks[2 * pr + 1][ch * 16 + 8]) = k1b;
+      // V transposed: column d of the pair's two keys packed in one dword
+      const uint32_t a[8] = {v0a.x, v0a.y, v0a.z, v0a.w, v0b.x, v0b.y, v0b.z, v0b.w};
+      const uint32_t b[8] = {v1a.x, v1a.y, v1a.z, v1a.w, v1b.x, v1b.y, v1b.z, v1b.w};
 #pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      const int item = tid + it * 256;
-      if (item < ITEMS) {
-        const int pr = item / NCH, ch = item % NCH;
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          *reinterpret_cast<uint4*>(&Ks[2 * pr + u][ch * 16]) = rk[it][u][0];
-          *reinterpret_cast<uint4*>(&Ks[2 * pr + u][ch * 16 + 8]) = rk[it][u][1];
-        }
-        // V transposed: column d of the pair's two keys packed in one dword
-        const uint32_t* a = reinterpret_cast<const uint32_t*>(&rv[it][0][0]);
-        const uint32_t* b = reinterpret_cast<const uint32_t*>(&rv[it][1][0]);
-#pragma unroll
-        for (int w = 0; w < 8; ++w) {
-          const uint32_t x0 = a[w], x1 = b[w];
-          // elements 2w, 2w+1 of the chunk
-          *reinterpret_cast<uint32_t*>(&Vt[ch * 16 + 2 * w][2 * pr]) = (x0 & 0xffffu) | (x1 << 16);
-          *reinterpret_cast<uint32_t*>(&Vt[ch * 16 + 2 * w + 1][2 * pr]) = (x0 >> 16) | (x1 & 0xffff0000u);
-        }
+      for (int w = 0; w < 8; ++w) {
+        // elements 2w, 2w+1 of the chunk
+        *reinterpret_cast<uint32_t*>(&Vt[ch * 16 + 2 * w][vt_col(ch, pr)]) = (a[w] & 0xffffu) | (b[w] << 16);
+        *reinterpret_cast<uint32_t*>(&Vt[ch * 16 + 2 * w + 1][vt_col(ch, pr)]) =
+            (a[w] >> 16) | (b[w] & 0xffff0000u);
       }
     }
   };
@@ -797,12 +814,17 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   for (int u = 0; u < DT; ++u) o[u] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_part = 0.f;
 
+  tload(0);
   gload(0);
+  tload(BKEY);
   for (int kb = 0; kb < kend; kb += BKEY) {
     __syncthreads();          // previous block's readers are done with LDS
     sstore();
     __syncthreads();
-    if (kb + BKEY < kend) gload(kb + BKEY);
+    if (kb + BKEY < kend) {
+      gload(kb + BKEY);
+      tload(kb + 2 * BKEY);
+    }
 
     // S^T tile t: lane holds S[query l16][key 16 t + 4 lg + r]
     floatx4_t st[4];
@@ -817,53 +839,80 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
           st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[p][s], st[t], 0, 0, 0);
       }
     }
-    // causal mask, block max
-    float bm = -INFINITY;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = kb + 16 * t + 4 * lg + r;
-        if (j > qpos || j >= kend) st[t][r] = -INFINITY;
-        bm = fmaxf(bm, st[t][r]);
-      }
-    bm = fmaxf(bm, __shfl_xor(bm, 16));
-    bm = fmaxf(bm, __shfl_xor(bm, 32));
-    const float m_new = fmaxf(m_run, bm);
-    const float corr = m_new == -INFINITY ? 1.f : __expf(m_run - m_new);
-    m_run = m_new;
-    l_part *= corr;
-    // probabilities, split into NT bf16 terms in the A-operand key order
+    // causal mask and block max, probabilities split into NT bf16 terms in the
+    // A-operand key order, and the rescale of the output rows.  Key blocks that
+    // every query of this wavefront sees whole (all but the diagonal and the last
+    // one) take the path without the mask and its -inf tests; a wavefront whose
+    // running maxima all stay put has correction factors of exactly 1 and skips
+    // the rescale.  Both paths give the same bits as the general one.
     bf16x8_t pf[NT][2];
+    auto softmax = [&](auto masked_t) {
+      constexpr bool MASKED = decltype(masked_t)::value;
+      float bm = -INFINITY;
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float sv = st[2 * c + (e >> 2)][e & 3];
-        float pv = sv == -INFINITY ? 0.f : __expf(sv - m_new);
-        l_part += pv;
+        for (int r = 0; r < 4; ++r) {
+          if (MASKED) {
+            const int j = kb + 16 * t + 4 * lg + r;
+            if (j > qpos || j >= kend) st[t][r] = -INFINITY;
+          }
+          bm = fmaxf(bm, st[t][r]);
+        }
+      bm = fmaxf(bm, __shfl_xor(bm, 16));
+      bm = fmaxf(bm, __shfl_xor(bm, 32));
+      const float m_old = m_run, m_new = fmaxf(m_old, bm);
+      m_run = m_new;
+      const bool grow = __any(m_new > m_old);
+      float pvs[16];
 #pragma unroll
-        for (int p = 0; p < NT; ++p) {
-          const bf16_t tb = f32_to_bf16(pv);
-          pf[p][c][e] = __builtin_bit_cast(__bf16, tb);
-          pv -= bf16_to_f32(tb);
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float sv = st[2 * c + (e >> 2)][e & 3];
+          float pv = MASKED && sv == -INFINITY ? 0.f : __expf(sv - m_new);
+          pvs[8 * c + e] = pv;
+#pragma unroll
+          for (int p = 0; p < NT; ++p) {
+            const bf16_t tb = f32_to_bf16(pv);
+            pf[p][c][e] = __builtin_bit_cast(__bf16, tb);
+            pv -= bf16_to_f32(tb);
+          }
+        }
+      // l = l corr + p_0 + ... + p_15, the first step fused (with corr = 1, as
+      // when no maximum grew, the fused step is the plain sum)
+      float corr = 1.f;
+      if (grow) {
+        corr = m_new == -INFINITY ? 1.f : __expf(m_old - m_new);
+        l_part = __builtin_fmaf(l_part, corr, pvs[0]);
+      } else {
+        l_part += pvs[0];
+      }
+#pragma unroll
+      for (int i = 1; i < 16; ++i) l_part += pvs[i];
+      if (grow) {
+        // the output rows (queries 4 lg + r) by their correction factors
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float cr = __shfl(corr, 4 * lg + r);
+#pragma unroll
+          for (int u = 0; u < DT; ++u) o[u][r] *= cr;
         }
       }
-    // rescale the output rows (queries 4 lg + r) by their correction factors
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float cr = __shfl(corr, 4 * lg + r);
-#pragma unroll
-      for (int u = 0; u < DT; ++u) o[u][r] *= cr;
-    }
+    };
+    if (kb + BKEY - 1 > p0 + qb + 16 * wave || kb + BKEY > kend)
+      softmax(std::true_type{});
+    else
+      softmax(std::false_type{});
     // O += P V: B operand = V^T rows d, keys in the same slot order as P
 #pragma unroll
     for (int u = 0; u < DT; ++u) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const bf16_t* vr = &Vt[16 * u + l16][32 * c + 4 * lg];
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+        // keys 32 c + 4 lg .. + 3 (pairs 16 c + 2 lg, + 1) and 16 further on
+        const bf16_t* vrow = &Vt[16 * u + l16][0];
+        const uint2 lo = *reinterpret_cast<const uint2*>(vrow + vt_col(u, 16 * c + 2 * lg));
+        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + vt_col(u, 16 * c + 2 * lg + 8));
         const uint4 w4 = make_uint4(lo.x, lo.y, hi.x, hi.y);
         const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, w4);
 #pragma unroll
@@ -916,7 +965,7 @@ static hipError_t attn_prefill_t(const float* qkv, int T, int p0, int Hq, KvLayo
 template <int HD>
 static hipError_t attn_prefill_mfma(const float* qkv, int T, int p0, int Hq, KvLayout kv,
                                     const ActBuf& out, int terms, hipStream_t s) {
-  const dim3 grid((T + 63) / 64, Hq);
+  const dim3 grid(((T + 63) / 64 * Hq + 7) / 8 * 8);
   const int cus = device_cus();
   switch (terms) {
     case 1: hipLaunchKernelGGL((k_attn_prefill_mfma<HD, 1>), grid, dim3(256), 0, s, qkv, T, p0, Hq, kv, out, cus); break;

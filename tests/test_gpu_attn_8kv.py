@@ -63,3 +63,27 @@ def test_decode_attention_8_kv_heads_graph_equals_eager(cuda_ok):
     a = _run(cfg, w, prompt, 8)
     b = _run(cfg, w, prompt, 8, graph=False)
     assert a[0] == b[0] and np.array_equal(a[1], b[1])
+
+
+# Prefill attention with 32 query heads and a chunk whose query-block count does
+# not divide the CU count: more (query block, head) pairs than CUs, so the
+# long/short pairing of causal walks reverses the block order for some heads and
+# not others, which must still cover every (head, query block) exactly once.
+# The fp32-cache case runs the vector kernel, the bf16 ones the matrix-core one.
+F32 = configs.ModelConfig(name="t_kv8_f32", key=97, n_layers=2, d_model=512, n_heads=32,
+                          n_kv_heads=8, head_dim=64, ffn_dim=768, vocab=1009,
+                          weight_dtype="f32", kv_dtype="f32", prompt_len=700, decode_steps=4)
+
+
+@pytest.mark.parametrize("name,P,chunk", [("hd128", 700, None), ("hd128", 1000, 640),
+                                          ("hd64", 700, None), ("f32", 700, None)])
+def test_prefill_attention_many_heads_ragged_blocks(cuda_ok, name, P, chunk):
+    cfg = F32 if name == "f32" else CFGS[name]
+    w = inputs.make_weights(cfg, gain_std=0.1)
+    prompt = inputs.make_prompt(cfg, P)
+    kw = {"max_seq": P + 16} if chunk is None else {"max_seq": P + 16, "prefill_chunk": chunk}
+    ids, lg = _run(cfg, w, prompt, 4, **kw)
+    rep = compare(ids, list(lg), *oracle_run(cfg, inputs.weights_f64(cfg, w), prompt, 4))
+    print(f"[prefill 32 heads] {name} P={P} chunk={chunk}: {rep.summary()}", flush=True)
+    assert rep.max_rel_err <= (1e-4 if cfg.weight_dtype == "f32" else 2e-2)
+    assert rep.strict_ids, rep.summary()
