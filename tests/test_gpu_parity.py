@@ -105,10 +105,14 @@ def test_ragged_prompts_chunks_and_pages(cuda_ok, P, chunk, page):
                                               (2100, 2200, 16), (2600, 4096, 64),
                                               (3000, 9000, 16), (5000, 16384, 128)])
 def test_long_capacity_decode_attention(cuda_ok, P, max_seq, page):
-    """The decode attention grid has one 64-position split per 64 positions of
-    capacity.  Up to 32 splits one workgroup per query head merges them; beyond
-    that, column-sliced workgroups do.  The cases give 32 and 33 splits (either
-    side of that switch), then 35, 64, 141 and 256, the most a launch accepts."""
+    """The decode attention has one 64-position sub-chunk per 64 positions of
+    capacity.  Up to 32 of them each is a split and the last split of a KV head
+    to finish merges them in the same launch; beyond that each split walks
+    ceil(sub-chunks / 32) consecutive sub-chunks under one online softmax (four
+    teams of four wavefronts) and the same merge applies.  The cases give 32 and
+    33 sub-chunks (either side of that switch), then 35 and 64 (two per split),
+    141 (five: one team takes two) and 256 (eight, two per team), the most a
+    launch accepts."""
     cfg = SMALL["gqa128_bf16"]
     prompt = inputs.make_prompt(cfg, P)
     rep, _, _ = run_parity(cfg, prompt, 12, gain_std=0.1, kv_page=page, max_seq=max_seq)
@@ -120,9 +124,10 @@ def test_long_capacity_decode_attention(cuda_ok, P, max_seq, page):
                                                    ("gqa64_bf16", 3000, 9000, 16),
                                                    ("mha64_f32", 2100, 2200, 16)])
 def test_long_capacity_decode_attention_head_dim_64(cuda_ok, name, P, max_seq, page):
-    """Past 32 splits at head dimension 64: each query head's merge takes two
-    32-column workgroups.  The bf16 cache runs on the matrix-core attention
-    kernel (33 and 141 splits), the fp32 cache on the vector one (35 splits)."""
+    """Past 32 sub-chunks at head dimension 64.  The bf16 cache runs on the
+    matrix-core attention with splits of several sub-chunks (33 and 141
+    sub-chunks); the fp32 cache on the vector kernel and the column-sliced merge
+    kernel (35 splits)."""
     cfg = SMALL[name]
     prompt = inputs.make_prompt(cfg, P)
     rep, _, _ = run_parity(cfg, prompt, 12, gain_std=0.1, kv_page=page, max_seq=max_seq)
