@@ -761,26 +761,30 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   static_assert(ITEMS <= 256, "one (pair, chunk) item per thread at most");
   const bool has_item = tid < ITEMS;
   const int pr = min(tid, ITEMS - 1) / NCH, ch = min(tid, ITEMS - 1) % NCH;
-  uint4 k0a, k0b, k1a, k1b, v0a, v0b, v1a, v1b;  // the pair's keys 0/1, 16-byte halves a/b
   const int kend = p0 + min(T, qb + BQ);      // keys [0, kend) are visible to this block
-  // Every load is unconditional, keys past the visible range clamped to the
-  // last visible one (finite values that the mask gives zero weight): a load
-  // under a branch makes the compiler wait for every load in flight where the
-  // paths join, which would expose each block's load latency.  The physical
-  // pages of a block's keys are requested one block before its keys and
-  // values, which keeps the page lookup off their path.
-  int pt0, pt1;
-  auto tload = [&](int kb) {
-    pt0 = kv.table[min(kb + 2 * pr, kend - 1) >> ps];
-    pt1 = kv.table[min(kb + 2 * pr + 1, kend - 1) >> ps];
+  // Two key blocks are in flight ahead of the one being multiplied (two
+  // register sets used in turn).  Every load is unconditional, keys past the
+  // visible range clamped to the last visible one (finite values that the mask
+  // gives zero weight): a load under a branch makes the compiler wait for every
+  // load in flight where the paths join, which would expose each block's load
+  // latency.  The physical pages of a block's keys are requested one block
+  // before its keys and values, which keeps the page lookup off their path.
+  auto tload = [&](int kb, int& pg0, int& pg1) {
+    pg0 = kv.table[min(kb + 2 * pr, kend - 1) >> ps];
+    pg1 = kv.table[min(kb + 2 * pr + 1, kend - 1) >> ps];
   };
   const bf16_t* kbase = base + (size_t)g * head_stride + ch * 16;
   const size_t pstride = (size_t)2 * Hkv * head_stride;  // elements per physical page
   const size_t vofs = (size_t)Hkv * head_stride;         // values after the keys
-  auto gload = [&](int kb) {
+  // a thread's (key pair, chunk) item of one key block, in one of two register
+  // sets: keys 0/1 and values 0/1 of the pair, 16-byte halves a/b
+  uint4 ka0a, ka0b, ka1a, ka1b, va0a, va0b, va1a, va1b;
+  uint4 kb0a, kb0b, kb1a, kb1b, vb0a, vb0b, vb1a, vb1b;
+  auto gload = [&](uint4& k0a, uint4& k0b, uint4& k1a, uint4& k1b, uint4& v0a, uint4& v0b,
+                   uint4& v1a, uint4& v1b, int kb, int pg0, int pg1) {
     const int j0 = min(kb + 2 * pr, kend - 1), j1 = min(kb + 2 * pr + 1, kend - 1);
-    const bf16_t* kp0 = kbase + (size_t)pt0 * pstride + (size_t)(j0 & (kv.page - 1)) * HD;
-    const bf16_t* kp1 = kbase + (size_t)pt1 * pstride + (size_t)(j1 & (kv.page - 1)) * HD;
+    const bf16_t* kp0 = kbase + (size_t)pg0 * pstride + (size_t)(j0 & (kv.page - 1)) * HD;
+    const bf16_t* kp1 = kbase + (size_t)pg1 * pstride + (size_t)(j1 & (kv.page - 1)) * HD;
     k0a = *reinterpret_cast<const uint4*>(kp0);
     k0b = *reinterpret_cast<const uint4*>(kp0 + 8);
     k1a = *reinterpret_cast<const uint4*>(kp1);
@@ -790,7 +794,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
     v1a = *reinterpret_cast<const uint4*>(kp1 + vofs);
     v1b = *reinterpret_cast<const uint4*>(kp1 + vofs + 8);
   };
-  auto sstore = [&]() {
+  auto sstore = [&](const uint4& k0a, const uint4& k0b, const uint4& k1a, const uint4& k1b,
+                    const uint4& v0a, const uint4& v0b, const uint4& v1a, const uint4& v1b) {
     if (has_item) {
       *reinterpret_cast<uint4*>(&Ks[2 * pr][ch * 16]) = k0a;
       *reinterpret_cast<uint4*>(&Ks[2 * pr][ch * 16 + 8]) = k0b;
@@ -814,18 +819,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
   for (int u = 0; u < DT; ++u) o[u] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_part = 0.f;
 
-  tload(0);
-  gload(0);
-  tload(BKEY);
-  for (int kb = 0; kb < kend; kb += BKEY) {
-    __syncthreads();          // previous block's readers are done with LDS
-    sstore();
-    __syncthreads();
-    if (kb + BKEY < kend) {
-      gload(kb + BKEY);
-      tload(kb + 2 * BKEY);
-    }
-
+  auto compute = [&](int kb) {
     // S^T tile t: lane holds S[query l16][key 16 t + 4 lg + r]
     floatx4_t st[4];
 #pragma unroll
@@ -920,7 +914,35 @@ __global__ __launch_bounds__(256) void k_attn_prefill_mfma(const float* __restri
           o[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf[p][c], vf, o[u], 0, 0, 0);
       }
     }
+  };
+
+  // blocks kb (set a) and kb + BKEY (set b) in turn; each step stores its set,
+  // refills it with the block two ahead and multiplies the stored block
+#define WICI_SET_A ka0a, ka0b, ka1a, ka1b, va0a, va0b, va1a, va1b
+#define WICI_SET_B kb0a, kb0b, kb1a, kb1b, vb0a, vb0b, vb1a, vb1b
+  int pa0, pa1, pb0, pb1;  // pages of the next block to load into set a / b
+  tload(0, pa0, pa1);
+  gload(WICI_SET_A, 0, pa0, pa1);
+  tload(BKEY, pb0, pb1);
+  gload(WICI_SET_B, BKEY, pb0, pb1);
+  tload(2 * BKEY, pa0, pa1);
+  for (int kb = 0; kb < kend; kb += 2 * BKEY) {
+    __syncthreads();          // previous block's readers are done with LDS
+    sstore(WICI_SET_A);
+    __syncthreads();
+    gload(WICI_SET_A, kb + 2 * BKEY, pa0, pa1);
+    tload(kb + 3 * BKEY, pb0, pb1);
+    compute(kb);
+    if (kb + BKEY >= kend) break;
+    __syncthreads();
+    sstore(WICI_SET_B);
+    __syncthreads();
+    gload(WICI_SET_B, kb + 3 * BKEY, pb0, pb1);
+    tload(kb + 4 * BKEY, pa0, pa1);
+    compute(kb + BKEY);
   }
+#undef WICI_SET_A
+#undef WICI_SET_B
 
   // ---- normalise and write: lane holds O[query 4 lg + r][d 16 u + l16] -----------
   float l_tot = l_part + __shfl_xor(l_part, 16);
