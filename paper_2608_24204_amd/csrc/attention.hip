@@ -682,8 +682,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(const float* __restrict__ 
 // ------------------------------------------------------------- prefill, MFMA
 // Flash attention on the matrix cores.  Block = 4 wavefronts = 64 query rows of
 // one query head (16 per wavefront); keys stream through LDS in blocks of 64
-// (K as [key][d], V transposed to [d][key]), the next block's loads in flight
-// while the current one is processed.  Per key block a wavefront computes
+// (K as [key][d], V transposed to [d][key]), the next two blocks' loads in
+// flight while the current one is processed.  Per key block a wavefront computes
 // S^T = K Q^T (so each lane ends up with 16 keys of one query, the row layout the
 // A operand of the next product needs), the online-softmax update, and
 // O += P V.  The query and the probabilities are fp32 values split into NT bf16
