@@ -306,11 +306,115 @@ __global__ __launch_bounds__(256) void k_rope_append(float* __restrict__ qkv, in
   }
 }
 
+// The same on 4-element slices (head dimension a multiple of 8), with every load
+// of a thread's slices (both K-range partials, cos and sin) issued before any is
+// used: the loop form above makes each of its ~14 iterations wait out its own
+// loads.  Slices past the end load a clamped index and store nothing.  Same
+// operations per element, so the results are bit-identical.
+template <typename KT, int NP, int MAXI>
+__global__ __launch_bounds__(256) void k_rope_append4(float* __restrict__ qkv, int p0, int Hq,
+                                                      const float* __restrict__ cos_t,
+                                                      const float* __restrict__ sin_t,
+                                                      KvLayout kv, const float* __restrict__ part,
+                                                      size_t p_split) {
+  const int t = blockIdx.x, pos = p0 + t, tid = threadIdx.x;
+  const int hd = kv.hd, half = hd >> 1, Hkv = kv.n_kv, q4 = half >> 2;
+  const int width = (Hq + 2 * Hkv) * hd;
+  float* row = qkv + (size_t)t * width;
+  const float* prow = part + (size_t)t * width;
+  auto ld4 = [&](int i) {  // the K-range partials of elements i .. i + 3, summed in order
+    float4 v = *reinterpret_cast<const float4*>(prow + i);
+#pragma unroll
+    for (int s = 1; s < NP; ++s) {
+      const float4 w = *reinterpret_cast<const float4*>(prow + (size_t)s * p_split + i);
+      v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+    }
+    return v;
+  };
+  KT* base = static_cast<KT*>(kv.base);
+  const int phys = kv.table[pos / kv.page], slot = pos % kv.page;
+  const int nrot = (Hq + Hkv) * q4, nval = Hkv * hd / 4;  // slices
+  float4 a[MAXI], b[MAXI], c[MAXI], sn[MAXI], v[MAXI];
+#pragma unroll
+  for (int k = 0; k < MAXI; ++k) {
+    const int i = min(tid + 256 * k, nrot - 1), h = i / q4, j = 4 * (i % q4);
+    a[k] = ld4(h * hd + j);
+    b[k] = ld4(h * hd + j + half);
+    c[k] = *reinterpret_cast<const float4*>(cos_t + (size_t)pos * half + j);
+    sn[k] = *reinterpret_cast<const float4*>(sin_t + (size_t)pos * half + j);
+    v[k] = ld4((Hq + Hkv) * hd + 4 * min(tid + 256 * k, nval - 1));
+  }
+  auto put = [&](KT* dst, float4 x) {
+    if constexpr (sizeof(KT) == 4) {
+      *reinterpret_cast<float4*>(dst) = x;
+    } else {
+      const uint2 u = make_uint2((uint32_t)f32_to_bf16(x.x) | ((uint32_t)f32_to_bf16(x.y) << 16),
+                                 (uint32_t)f32_to_bf16(x.z) | ((uint32_t)f32_to_bf16(x.w) << 16));
+      *reinterpret_cast<uint2*>(dst) = u;
+    }
+  };
+#pragma unroll
+  for (int k = 0; k < MAXI; ++k) {
+    const int i = tid + 256 * k;
+    if (i < nrot) {
+      const int h = i / q4, j = 4 * (i % q4);
+      float4 ra, rb;
+      ra.x = a[k].x * c[k].x - b[k].x * sn[k].x; rb.x = a[k].x * sn[k].x + b[k].x * c[k].x;
+      ra.y = a[k].y * c[k].y - b[k].y * sn[k].y; rb.y = a[k].y * sn[k].y + b[k].y * c[k].y;
+      ra.z = a[k].z * c[k].z - b[k].z * sn[k].z; rb.z = a[k].z * sn[k].z + b[k].z * c[k].z;
+      ra.w = a[k].w * c[k].w - b[k].w * sn[k].w; rb.w = a[k].w * sn[k].w + b[k].w * c[k].w;
+      if (h < Hq) {
+        *reinterpret_cast<float4*>(row + h * hd + j) = ra;
+        *reinterpret_cast<float4*>(row + h * hd + j + half) = rb;
+      } else {
+        KT* dst = base + (((size_t)phys * 2 + 0) * Hkv + (h - Hq)) * kv.page * hd + (size_t)slot * hd;
+        put(dst + j, ra);
+        put(dst + j + half, rb);
+      }
+    }
+    if (i < nval) {
+      const int g = (4 * i) / hd, e = (4 * i) % hd;
+      KT* dst = base + (((size_t)phys * 2 + 1) * Hkv + g) * kv.page * hd + (size_t)slot * hd;
+      put(dst + e, v[k]);
+    }
+  }
+}
+
+template <typename KT>
+static bool rope_append4(float* qkv, int T, int p0, int Hq, const float* cos_t,
+                         const float* sin_t, KvLayout kv, hipStream_t st, const float* part,
+                         int nsplit, size_t p_split) {
+  constexpr int MAXI = 4;
+  const int hd = kv.hd;
+  if (!part || hd % 8 || p_split % 4 || (Hq + kv.n_kv) * (hd / 8) > 256 * MAXI ||
+      kv.n_kv * hd / 4 > 256 * MAXI)
+    return false;
+  switch (nsplit) {
+    case 2:
+      hipLaunchKernelGGL((k_rope_append4<KT, 2, MAXI>), dim3(T), dim3(256), 0, st, qkv, p0, Hq,
+                         cos_t, sin_t, kv, part, p_split);
+      return true;
+    case 3:
+      hipLaunchKernelGGL((k_rope_append4<KT, 3, MAXI>), dim3(T), dim3(256), 0, st, qkv, p0, Hq,
+                         cos_t, sin_t, kv, part, p_split);
+      return true;
+    case 4:
+      hipLaunchKernelGGL((k_rope_append4<KT, 4, MAXI>), dim3(T), dim3(256), 0, st, qkv, p0, Hq,
+                         cos_t, sin_t, kv, part, p_split);
+      return true;
+    default:
+      return false;
+  }
+}
+
 hipError_t launch_rope_append(bool kv_bf16, float* qkv, int T, int p0, int Hq,
                               const float* cos_t, const float* sin_t, KvLayout kv,
                               hipStream_t st, const float* part, int nsplit, size_t p_split) {
   if (nsplit < 1 || (nsplit > 1 && !part)) return hipErrorInvalidValue;
   if (nsplit == 1) part = nullptr;
+  if (kv_bf16 ? rope_append4<bf16_t>(qkv, T, p0, Hq, cos_t, sin_t, kv, st, part, nsplit, p_split)
+              : rope_append4<float>(qkv, T, p0, Hq, cos_t, sin_t, kv, st, part, nsplit, p_split))
+    return hipGetLastError();
   if (kv_bf16)
     hipLaunchKernelGGL(k_rope_append<bf16_t>, dim3(T), dim3(256), 0, st, qkv, p0, Hq, cos_t,
                        sin_t, kv, part, nsplit, p_split);
