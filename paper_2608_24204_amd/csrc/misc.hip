@@ -143,8 +143,54 @@ __global__ __launch_bounds__(256) void k_rmsnorm_rows(const float* __restrict__ 
   }
 }
 
+// The same for rows of NV * 1024 values: the row and the gain are loaded at once
+// and kept in registers (the loop form waits for each slice in turn, then reads
+// the row again).  Same elements per thread and order of operations, so the
+// results are bit-identical.
+template <int NV>
+__global__ __launch_bounds__(256) void k_rmsnorm_rows_reg(const float* __restrict__ x,
+                                                          const float* __restrict__ g, float eps,
+                                                          int d, ActBuf y) {
+  __shared__ float red[4];
+  const float4* xr = reinterpret_cast<const float4*>(x + (size_t)blockIdx.x * d);
+  const size_t yr = (size_t)blockIdx.x * d;
+  const int tid = threadIdx.x;
+  float4 v[NV], w[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = xr[tid + 256 * i];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) w[i] = reinterpret_cast<const float4*>(g)[tid + 256 * i];
+  // the loop form's sum of squares as that kernel is compiled (y^2 rounded, then
+  // x, z and w fused in), written out so that the compiler cannot fuse it
+  // differently here: the same bits at every row length
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    ss += __builtin_fmaf(v[i].w, v[i].w,
+                         __builtin_fmaf(v[i].z, v[i].z, __builtin_fmaf(v[i].x, v[i].x, v[i].y * v[i].y)));
+  const float r = 1.0f / sqrtf(block256_sum(ss, red) / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const size_t k = yr + 4 * (tid + 256 * i);
+    store_act(y, k + 0, v[i].x * r * w[i].x);
+    store_act(y, k + 1, v[i].y * r * w[i].y);
+    store_act(y, k + 2, v[i].z * r * w[i].z);
+    store_act(y, k + 3, v[i].w * r * w[i].w);
+  }
+}
+
 hipError_t launch_rmsnorm_rows(const float* x, const float* gain, float eps, int T, int d,
                                const ActBuf& y, hipStream_t st) {
+  if (d % 1024 == 0 && d / 1024 >= 1 && d / 1024 <= 8) {
+    switch (d / 1024) {
+#define WICI_RN(NV)                                                                              \
+  case NV:                                                                                       \
+    hipLaunchKernelGGL((k_rmsnorm_rows_reg<NV>), dim3(T), dim3(256), 0, st, x, gain, eps, d, y); \
+    return hipGetLastError();
+      WICI_RN(1) WICI_RN(2) WICI_RN(3) WICI_RN(4) WICI_RN(5) WICI_RN(6) WICI_RN(7) WICI_RN(8)
+#undef WICI_RN
+    }
+  }
   hipLaunchKernelGGL(k_rmsnorm_rows, dim3(T), dim3(256), 0, st, x, gain, eps, d, y);
   return hipGetLastError();
 }
