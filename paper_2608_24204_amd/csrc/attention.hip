@@ -420,10 +420,50 @@ __global__ __launch_bounds__(HD) void k_attn_merge_batch(const float* __restrict
   __shared__ float red[HD / 64];
   const int h = blockIdx.x, b = blockIdx.y, Hq = gridDim.x;
   const int d = threadIdx.x, lane = d & 63, wv = d >> 6;
-  const int pos = static_cast<const DecodeState*>(seqs[b].state)->pos;
-  const int active = (pos + kChunk) / kChunk;
   const size_t head = (size_t)b * Hq + h;
   const float* ml = part_ml + head * nsplit * 2;
+  const float* po = part_o + head * nsplit * HD + d;
+  // Up to 32 splits this thread's column of every split is requested with the
+  // position, before the split count is known (clamped; the unused ones are
+  // dropped), so the merge is one memory round trip; the arithmetic and its
+  // order are the loop form's below.
+  constexpr int PS = 32;
+  if (nsplit <= PS && HD >= PS) {
+    float pv[PS];
+#pragma unroll
+    for (int s = 0; s < PS; ++s) pv[s] = po[(size_t)min(s, nsplit - 1) * HD];
+    const float2 mlv = *reinterpret_cast<const float2*>(ml + 2 * min(d, nsplit - 1));
+    const int pos = static_cast<const DecodeState*>(seqs[b].state)->pos;
+    const int active = (pos + kChunk) / kChunk;
+    float mloc = d < active ? mlv.x : -INFINITY;
+    mloc = wave_max(mloc);
+    if (lane == 0) red[wv] = mloc;
+    __syncthreads();
+    float M = red[0];
+#pragma unroll
+    for (int i = 1; i < HD / 64; ++i) M = fmaxf(M, red[i]);
+    float lsum = 0.f;
+    if (d < active) {
+      const float e = __expf(mlv.x - M);
+      w[d] = e;
+      lsum += e * mlv.y;
+    }
+    lsum = wave_sum(lsum);
+    __syncthreads();
+    if (lane == 0) red[wv] = lsum;
+    __syncthreads();
+    float L = 0.f;
+#pragma unroll
+    for (int i = 0; i < HD / 64; ++i) L += red[i];
+    float o = 0.f;
+#pragma unroll
+    for (int s = 0; s < PS; ++s)
+      if (s < active) o += w[s] * pv[s];
+    store_act(out, ((size_t)b * Hq + h) * HD + d, o / L);
+    return;
+  }
+  const int pos = static_cast<const DecodeState*>(seqs[b].state)->pos;
+  const int active = (pos + kChunk) / kChunk;
   float mloc = -INFINITY;
   for (int s = d; s < active; s += HD) mloc = fmaxf(mloc, ml[2 * s]);
   mloc = wave_max(mloc);
@@ -445,7 +485,6 @@ __global__ __launch_bounds__(HD) void k_attn_merge_batch(const float* __restrict
   float L = 0.f;
 #pragma unroll
   for (int i = 0; i < HD / 64; ++i) L += red[i];
-  const float* po = part_o + head * nsplit * HD + d;
   float o = 0.f;
   for (int s = 0; s < active; ++s) o += w[s] * po[(size_t)s * HD];
   store_act(out, ((size_t)b * Hq + h) * HD + d, o / L);
