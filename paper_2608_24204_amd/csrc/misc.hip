@@ -367,8 +367,10 @@ __global__ __launch_bounds__(256) void k_rope_append4(float* __restrict__ qkv, i
   const int hd = kv.hd, half = hd >> 1, Hkv = kv.n_kv, q4 = half >> 2;
   const int width = (Hq + 2 * Hkv) * hd;
   float* row = qkv + (size_t)t * width;
-  const float* prow = part + (size_t)t * width;
-  auto ld4 = [&](int i) {  // the K-range partials of elements i .. i + 3, summed in order
+  // the projection's row itself (rotated in place: every slice is read before
+  // any is written, each by the thread that writes it) or its K-range partials
+  const float* prow = part ? part + (size_t)t * width : row;
+  auto ld4 = [&](int i) {  // elements i .. i + 3, the K-range partials summed in order
     float4 v = *reinterpret_cast<const float4*>(prow + i);
 #pragma unroll
     for (int s = 1; s < NP; ++s) {
@@ -432,10 +434,14 @@ static bool rope_append4(float* qkv, int T, int p0, int Hq, const float* cos_t,
                          int nsplit, size_t p_split) {
   constexpr int MAXI = 4;
   const int hd = kv.hd;
-  if (!part || hd % 8 || p_split % 4 || (Hq + kv.n_kv) * (hd / 8) > 256 * MAXI ||
+  if (hd % 8 || p_split % 4 || (Hq + kv.n_kv) * (hd / 8) > 256 * MAXI ||
       kv.n_kv * hd / 4 > 256 * MAXI)
     return false;
-  switch (nsplit) {
+  switch (part ? nsplit : 1) {
+    case 1:
+      hipLaunchKernelGGL((k_rope_append4<KT, 1, MAXI>), dim3(T), dim3(256), 0, st, qkv, p0, Hq,
+                         cos_t, sin_t, kv, (const float*)nullptr, p_split);
+      return true;
     case 2:
       hipLaunchKernelGGL((k_rope_append4<KT, 2, MAXI>), dim3(T), dim3(256), 0, st, qkv, p0, Hq,
                          cos_t, sin_t, kv, part, p_split);
