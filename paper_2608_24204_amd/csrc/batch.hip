@@ -60,9 +60,92 @@ __global__ __launch_bounds__(256) void k_rope_append_batch(float* __restrict__ q
   }
 }
 
+// The same on 4-element slices (head dimension a multiple of 8) with every load
+// of a thread's slices issued before any is used (the loop form above waits out
+// each iteration's loads); rotated in place, each slice read and written by one
+// thread.  Same operations per element: bit-identical results.
+template <typename KT, int MAXI>
+__global__ __launch_bounds__(256) void k_rope_append_batch4(float* __restrict__ qkv, int Hq,
+                                                            const float* __restrict__ cos_t,
+                                                            const float* __restrict__ sin_t,
+                                                            const SeqDesc* __restrict__ seqs,
+                                                            int layer, KvLayout kv, float q_scale) {
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const SeqDesc sd = seqs[b];
+  const int hd = kv.hd, half = hd >> 1, Hkv = kv.n_kv, q4 = half >> 2;
+  float* row = qkv + (size_t)b * (Hq + 2 * Hkv) * hd;
+  const int nrot = (Hq + Hkv) * q4, nval = Hkv * hd / 4;  // slices
+  float4 a[MAXI], bb[MAXI], v[MAXI];
+#pragma unroll
+  for (int k = 0; k < MAXI; ++k) {
+    const int i = min(tid + 256 * k, nrot - 1), h = i / q4, j = 4 * (i % q4);
+    a[k] = *reinterpret_cast<const float4*>(row + h * hd + j);
+    bb[k] = *reinterpret_cast<const float4*>(row + h * hd + j + half);
+    v[k] = *reinterpret_cast<const float4*>(row + (Hq + Hkv) * hd + 4 * min(tid + 256 * k, nval - 1));
+  }
+  const int pos = static_cast<const DecodeState*>(sd.state)->pos;
+  KT* base = reinterpret_cast<KT*>(static_cast<char*>(sd.kv) + (size_t)layer * sd.kv_layer_stride);
+  const int phys = sd.table[pos / kv.page], slot = pos % kv.page;
+  float4 c[MAXI], sn[MAXI];
+#pragma unroll
+  for (int k = 0; k < MAXI; ++k) {
+    const int i = min(tid + 256 * k, nrot - 1), j = 4 * (i % q4);
+    c[k] = *reinterpret_cast<const float4*>(cos_t + (size_t)pos * half + j);
+    sn[k] = *reinterpret_cast<const float4*>(sin_t + (size_t)pos * half + j);
+  }
+  auto put = [&](KT* dst, float4 x) {
+    if constexpr (sizeof(KT) == 4) {
+      *reinterpret_cast<float4*>(dst) = x;
+    } else {
+      const uint2 u = make_uint2((uint32_t)f32_to_bf16(x.x) | ((uint32_t)f32_to_bf16(x.y) << 16),
+                                 (uint32_t)f32_to_bf16(x.z) | ((uint32_t)f32_to_bf16(x.w) << 16));
+      *reinterpret_cast<uint2*>(dst) = u;
+    }
+  };
+#pragma unroll
+  for (int k = 0; k < MAXI; ++k) {
+    const int i = tid + 256 * k;
+    if (i < nrot) {
+      const int h = i / q4, j = 4 * (i % q4);
+      float4 ra, rb;
+      ra.x = a[k].x * c[k].x - bb[k].x * sn[k].x; rb.x = a[k].x * sn[k].x + bb[k].x * c[k].x;
+      ra.y = a[k].y * c[k].y - bb[k].y * sn[k].y; rb.y = a[k].y * sn[k].y + bb[k].y * c[k].y;
+      ra.z = a[k].z * c[k].z - bb[k].z * sn[k].z; rb.z = a[k].z * sn[k].z + bb[k].z * c[k].z;
+      ra.w = a[k].w * c[k].w - bb[k].w * sn[k].w; rb.w = a[k].w * sn[k].w + bb[k].w * c[k].w;
+      if (h < Hq) {
+        float* z = row + h * hd;
+        *reinterpret_cast<float4*>(z + j) =
+            make_float4(ra.x * q_scale, ra.y * q_scale, ra.z * q_scale, ra.w * q_scale);
+        *reinterpret_cast<float4*>(z + j + half) =
+            make_float4(rb.x * q_scale, rb.y * q_scale, rb.z * q_scale, rb.w * q_scale);
+      } else {
+        KT* dst = base + (((size_t)phys * 2 + 0) * Hkv + (h - Hq)) * kv.page * hd + (size_t)slot * hd;
+        put(dst + j, ra);
+        put(dst + j + half, rb);
+      }
+    }
+    if (i < nval) {
+      const int g = (4 * i) / hd, e = (4 * i) % hd;
+      KT* dst = base + (((size_t)phys * 2 + 1) * Hkv + g) * kv.page * hd + (size_t)slot * hd;
+      put(dst + e, v[k]);
+    }
+  }
+}
+
 hipError_t launch_rope_append_batch(bool kv_bf16, float* qkv, int B, int Hq, const float* cos_t,
                                     const float* sin_t, const SeqDesc* seqs, int layer,
                                     KvLayout kv, float q_scale, hipStream_t st) {
+  constexpr int MAXI = 4;
+  if (kv.hd % 8 == 0 && (Hq + kv.n_kv) * (kv.hd / 8) <= 256 * MAXI &&
+      kv.n_kv * kv.hd / 4 <= 256 * MAXI) {
+    if (kv_bf16)
+      hipLaunchKernelGGL((k_rope_append_batch4<bf16_t, MAXI>), dim3(B), dim3(256), 0, st, qkv,
+                         Hq, cos_t, sin_t, seqs, layer, kv, q_scale);
+    else
+      hipLaunchKernelGGL((k_rope_append_batch4<float, MAXI>), dim3(B), dim3(256), 0, st, qkv,
+                         Hq, cos_t, sin_t, seqs, layer, kv, q_scale);
+    return hipGetLastError();
+  }
   if (kv_bf16)
     hipLaunchKernelGGL(k_rope_append_batch<bf16_t>, dim3(B), dim3(256), 0, st, qkv, Hq, cos_t,
                        sin_t, seqs, layer, kv, q_scale);
