@@ -127,6 +127,26 @@ __device__ __forceinline__ void store_act(const ActBuf& a, size_t idx, float v) 
   }
 }
 
+// Four consecutive values (idx a multiple of 4): the same terms as four
+// store_act calls, written as one 8-byte store per plane (16 bytes for fp32).
+__device__ __forceinline__ void store_act4(const ActBuf& a, size_t idx, float4 v) {
+  if (a.nt == 0) {
+    *reinterpret_cast<float4*>(a.f32 + idx) = v;
+    return;
+  }
+  float r[4] = {v.x, v.y, v.z, v.w};
+  for (int p = 0; p < a.nt; ++p) {
+    bf16_t t[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      t[e] = f32_to_bf16(r[e]);
+      r[e] -= bf16_to_f32(t[e]);
+    }
+    *reinterpret_cast<uint2*>(a.planes + p * a.plane_stride + idx) =
+        make_uint2((uint32_t)t[0] | ((uint32_t)t[1] << 16), (uint32_t)t[2] | ((uint32_t)t[3] << 16));
+  }
+}
+
 // Greedy-argmax order: larger value wins, lower index wins among equal values.
 __device__ __forceinline__ bool am_better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);

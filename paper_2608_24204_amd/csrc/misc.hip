@@ -172,10 +172,8 @@ __global__ __launch_bounds__(256) void k_rmsnorm_rows_reg(const float* __restric
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const size_t k = yr + 4 * (tid + 256 * i);
-    store_act(y, k + 0, v[i].x * r * w[i].x);
-    store_act(y, k + 1, v[i].y * r * w[i].y);
-    store_act(y, k + 2, v[i].z * r * w[i].z);
-    store_act(y, k + 3, v[i].w * r * w[i].w);
+    store_act4(y, k, make_float4(v[i].x * r * w[i].x, v[i].y * r * w[i].y, v[i].z * r * w[i].z,
+                                 v[i].w * r * w[i].w));
   }
 }
 
@@ -269,10 +267,8 @@ __global__ __launch_bounds__(256) void k_resid_sum_rmsnorm_reg(float* __restrict
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const size_t k = yr + 4 * (tid + 256 * i);
-    store_act(y, k + 0, v[i].x * r * w[i].x);
-    store_act(y, k + 1, v[i].y * r * w[i].y);
-    store_act(y, k + 2, v[i].z * r * w[i].z);
-    store_act(y, k + 3, v[i].w * r * w[i].w);
+    store_act4(y, k, make_float4(v[i].x * r * w[i].x, v[i].y * r * w[i].y, v[i].z * r * w[i].z,
+                                 v[i].w * r * w[i].w));
   }
 }
 
